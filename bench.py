@@ -1,0 +1,219 @@
+#!/usr/bin/env python3
+"""Benchmark of the tiled symmetric InfoNCE loss (forward + backward) on one MI355X.
+
+A step is one full pass of the loss: infcl_fwd (similarity tiles, online
+row/column log-sum-exp, per-sample terms, loss) followed by infcl_bwd (both
+gradient sweeps and dscale) over one batch of synthetic CLIP-shaped embeddings
+already resident in HBM.  The metric is similarity entries per second,
+b^2 / (time of one forward + backward).
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+
+Prints one JSON line.  Only one GPU is used; --gpus above 1 exits with a message.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+BF16_PEAK = 2.5e15      # MI355X dense bf16 MFMA, FLOP/s
+FP32_MFMA_PEAK = 157.3e12
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=2, help="workload configuration 1..5 (default 2)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-b", type=int, default=12288)
+    return ap.parse_args()
+
+
+def source_hash(*names) -> str:
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2410_17243_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel: str, workload: str, src: str):
+    """HBM bytes per launch from the committed rocprofv3 counter runs, or None
+    when absent or taken on a different kernel source."""
+    try:
+        with open(PROFILE_TRAFFIC) as f:
+            t = json.load(f)
+        e = t[kernel]
+        if e.get("source_hash") != src or e.get("workload") != workload:
+            return None
+        return e["bytes_per_launch"]
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(cfg, sample_b):
+    """The fp64 oracle (as it stands) on a bounded sample of the same workload."""
+    import oracle
+    from oracle.infonce import _threads
+    from paper_2410_17243_amd import synth
+
+    img, txt = synth.clip_pairs(sample_b, cfg["d"], cfg["sigma"], seed=0, dtype=cfg["dtype"])
+    I = synth.as_f64(img, cfg["dtype"])
+    T = synth.as_f64(txt, cfg["dtype"])
+    s = float(__import__("numpy").float32(cfg["scale"]))
+    t0 = time.perf_counter()
+    oracle.forward_backward(I, T, s)
+    dt = time.perf_counter() - t0
+    return {
+        "value": sample_b * sample_b / dt,
+        "unit": "entries/s",
+        "cores": _threads(),
+        "kind": "oracle",
+        "sample": f"full fp64 oracle forward+backward at b={sample_b} (same generator, d={cfg['d']}, "
+                  f"sigma={cfg['sigma']}, s={cfg['scale']}, seed 0): {dt:.2f} s",
+    }
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {a.gpus}); this build has no multi-GPU path.",
+              file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2410_17243_amd as infcl
+    from paper_2410_17243_amd import synth
+
+    cfg = synth.CONFIGS[a.config]
+    b, d, dt_name = cfg["b"], cfg["d"], cfg["dtype"]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    img_np, txt_np = synth.clip_pairs(b, d, cfg["sigma"], seed=0, dtype=dt_name)
+    if dt_name == "bf16":
+        img = torch.from_numpy(img_np.view(np.int16)).view(torch.bfloat16).to(dev)
+        txt = torch.from_numpy(txt_np.view(np.int16)).view(torch.bfloat16).to(dev)
+    else:
+        img = torch.from_numpy(img_np).to(dev)
+        txt = torch.from_numpy(txt_np).to(dev)
+    del img_np, txt_np
+    scale = torch.tensor([cfg["scale"]], dtype=torch.float32, device=dev).reshape(())
+
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats(dev)
+    base_mem = torch.cuda.memory_allocated(dev)
+    # outputs and workspace, allocated once (torch owns every buffer)
+    ws = infcl.workspace_for(img)
+    loss = torch.empty((), dtype=torch.float32, device=dev)
+    loss64 = torch.empty((), dtype=torch.float64, device=dev)
+    lse_r = torch.empty(b, dtype=torch.float32, device=dev)
+    lse_c = torch.empty(b, dtype=torch.float32, device=dev)
+    aux = torch.empty(3 * b, dtype=torch.float32, device=dev)
+    dimg = torch.empty((b, d), dtype=torch.float32, device=dev)
+    dtxt = torch.empty((b, d), dtype=torch.float32, device=dev)
+    dscale = torch.empty((), dtype=torch.float32, device=dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        infcl.infcl_fwd(img, txt, scale, loss, loss64, lse_r, lse_c, aux, ws)
+        if ev is not None:
+            ev[1].record()
+        infcl.infcl_bwd(img, txt, scale, lse_r, lse_c, aux, None, dimg, dtxt, dscale, ws)
+        if ev is not None:
+            ev[2].record()
+
+    step()
+    torch.cuda.synchronize()
+    peak_bytes = torch.cuda.max_memory_allocated(dev)
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(a.steps)]
+    stream = torch.cuda.current_stream(dev)  # the stream the library launches on
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(a.steps):
+        step(evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    fwd_ms = [e[0].elapsed_time(e[1]) for e in evs]
+    bwd_ms = [e[1].elapsed_time(e[2]) for e in evs]
+    step_ms = [e[0].elapsed_time(e[2]) for e in evs]
+    gpu_total_ms = evs[0][0].elapsed_time(evs[-1][2])
+    ms_per_step = gpu_total_ms / a.steps
+    ms_wall = wall * 1e3 / a.steps
+    assert math.isfinite(float(loss64.item())), "non-finite loss"
+
+    entries = float(b) * float(b)
+    value = entries / (ms_per_step * 1e-3)
+    bwd_launch_ms = sum(bwd_ms) / len(bwd_ms) / 2.0   # two bwd_sweep launches per infcl_bwd call
+    fwd_launch_ms = sum(fwd_ms) / len(fwd_ms)
+    peak = BF16_PEAK if dt_name == "bf16" else FP32_MFMA_PEAK
+    alg_bwd_launch = 3.0 * entries * d      # half of the 6 b^2 d algorithmic backward flops
+    alg_fwd_launch = 2.0 * entries * d
+    achieved = alg_bwd_launch / (bwd_launch_ms * 1e-3)
+    workload = (f"symmetric InfoNCE fwd+bwd, b={b} d={d} {dt_name} embeddings, sigma={cfg['sigma']}, "
+                f"s={cfg['scale']} (config {a.config})")
+    src = source_hash("bwd.hip", "common.hpp")
+    traffic = load_traffic("bwd_sweep", workload, src)
+
+    out = {
+        "metric": "similarity entries/s (b^2 per forward+backward pass)",
+        "value": value,
+        "unit": "entries/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dt_name,
+        "data": "synthetic (seeded CLIP-shaped unit-norm pairs; no dataset)",
+        "config": {"workload": workload, "b": b, "d": d, "input_dtype": dt_name, "sigma": cfg["sigma"],
+                   "scale": cfg["scale"], "seed": 0},
+        "mfma_frac_algorithmic": 8.0 * entries * d / (ms_per_step * 1e-3) / peak,
+        "mfma_frac_executed": 10.0 * entries * d / (ms_per_step * 1e-3) / peak,
+        "fwd_ms": fwd_launch_ms,
+        "bwd_ms": 2.0 * bwd_launch_ms,
+        "ms_per_step_host_wall": ms_wall,
+        "step_ms_min": min(step_ms),
+        "peak_hbm_bytes": int(peak_bytes - base_mem + (img.numel() + txt.numel()) * img.element_size()),
+        "roofline": {
+            "kernel": "bwd_sweep (one of the two backward launches)",
+            "bound": "mfma",
+            "achieved": achieved / 1e12,
+            "peak": peak / 1e12,
+            "unit": "TFLOP/s",
+            "frac": achieved / peak,
+            "traffic": traffic,
+            "algorithmic_flops_per_launch": alg_bwd_launch,
+            "avg_launch_ms": bwd_launch_ms,
+            "fwd_sweep": {"achieved": alg_fwd_launch / (fwd_launch_ms * 1e-3) / 1e12,
+                          "frac": alg_fwd_launch / (fwd_launch_ms * 1e-3) / peak, "avg_launch_ms": fwd_launch_ms},
+        },
+        "cpu_baseline": None,
+    }
+    if not a.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, min(a.cpu_sample_b, b))
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,115 @@
+// C ABI of the tiled contrastive loss: argument validation, workspace layout,
+// grid selection and launches on the caller's stream.  No allocation, no host
+// synchronisation, no global mutable state.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/infcl.h"
+
+namespace infcl {
+int launch_fwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale, float* loss,
+               double* loss64, float* lse_r, float* lse_c, float* aux, char* ws, hipStream_t stream, int Pr, int Pc,
+               float* rowR, float* rowL, float* colR, float* colL, float* udiag, double* partial);
+int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale,
+               const float* lse_r, const float* lse_c, const float* aux, const float* dloss, float* dimg, float* dtxt,
+               float* dscale, double* ds_part, hipStream_t stream);
+bool bwd_supported(int64_t d, int dtype);
+}  // namespace infcl
+
+namespace {
+
+constexpr int64_t kMaxB = (int64_t)1 << 30;
+
+struct Layout {
+  int Pr, Pc;
+  size_t rowR, rowL, colR, colL, udiag, fwd_part, bwd_part, total;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Forward grid: Pc column groups (one per XCD when there are enough column
+// tiles) times Pr row groups, about two workgroups per compute unit.
+Layout make_layout(int64_t b) {
+  Layout L;
+  const int64_t nRT = (b + 63) / 64, nCT = (b + 255) / 256;
+  L.Pc = (int)(nCT < 8 ? nCT : 8);
+  L.Pr = (int)(nRT < 64 ? nRT : 64);
+  size_t off = 0;
+  const size_t fb = (size_t)b * sizeof(float);
+  L.rowR = off; off = align256(off + (size_t)L.Pc * 4 * fb);
+  L.rowL = off; off = align256(off + (size_t)L.Pc * 4 * fb);
+  L.colR = off; off = align256(off + (size_t)L.Pr * fb);
+  L.colL = off; off = align256(off + (size_t)L.Pr * fb);
+  L.udiag = off; off = align256(off + fb);
+  L.fwd_part = off; off = align256(off + (size_t)((b + 255) / 256) * sizeof(double));
+  L.bwd_part = off; off = align256(off + (size_t)2 * ((b + 127) / 128) * sizeof(double));
+  L.total = off;
+  return L;
+}
+
+bool aligned(const void* p, size_t a) { return p != nullptr && ((uintptr_t)p % a) == 0; }
+
+bool shape_ok(int64_t b, int64_t d, int dtype) { return b >= 1 && d >= 1 && (dtype == INFCL_BF16 || dtype == INFCL_F32); }
+
+bool shape_supported(int64_t b, int64_t d, int dtype) { return b <= kMaxB && infcl::bwd_supported(d, dtype); }
+
+}  // namespace
+
+extern "C" {
+
+infcl_status infcl_workspace_size(int64_t b, int64_t d, int dtype, size_t* bytes) {
+  if (bytes == nullptr || !shape_ok(b, d, dtype)) return INFCL_ERR_INVALID;
+  if (!shape_supported(b, d, dtype)) return INFCL_ERR_UNSUPPORTED;
+  *bytes = make_layout(b).total;
+  return INFCL_OK;
+}
+
+infcl_status infcl_fwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale,
+                       float* loss, double* loss64, float* lse_r, float* lse_c, float* aux, void* workspace,
+                       size_t ws_bytes, void* stream) {
+  if (!shape_ok(b, d, dtype)) return INFCL_ERR_INVALID;
+  if (!aligned(img, 16) || !aligned(txt, 16) || !aligned(scale, 4) || !aligned(loss, 4) || !aligned(lse_r, 16) ||
+      !aligned(lse_c, 16) || !aligned(aux, 16) || !aligned(workspace, 256))
+    return INFCL_ERR_INVALID;
+  if (loss64 != nullptr && ((uintptr_t)loss64 % 8) != 0) return INFCL_ERR_INVALID;
+  if (!shape_supported(b, d, dtype)) return INFCL_ERR_UNSUPPORTED;
+  const Layout L = make_layout(b);
+  if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
+  char* ws = (char*)workspace;
+  int rc = infcl::launch_fwd(img, txt, b, d, dtype, scale, loss, loss64, lse_r, lse_c, aux, ws, (hipStream_t)stream,
+                             L.Pr, L.Pc, (float*)(ws + L.rowR), (float*)(ws + L.rowL), (float*)(ws + L.colR),
+                             (float*)(ws + L.colL), (float*)(ws + L.udiag), (double*)(ws + L.fwd_part));
+  return rc == 0 ? INFCL_OK : INFCL_ERR_HIP;
+}
+
+infcl_status infcl_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale,
+                       const float* lse_r, const float* lse_c, const float* aux, const float* dloss, float* dimg,
+                       float* dtxt, float* dscale, void* workspace, size_t ws_bytes, void* stream) {
+  if (!shape_ok(b, d, dtype)) return INFCL_ERR_INVALID;
+  if (!aligned(img, 16) || !aligned(txt, 16) || !aligned(scale, 4) || !aligned(lse_r, 16) || !aligned(lse_c, 16) ||
+      !aligned(aux, 16) || !aligned(dimg, 16) || !aligned(dtxt, 16) || !aligned(dscale, 4) ||
+      !aligned(workspace, 256))
+    return INFCL_ERR_INVALID;
+  if (dloss != nullptr && ((uintptr_t)dloss % 4) != 0) return INFCL_ERR_INVALID;
+  if (!shape_supported(b, d, dtype)) return INFCL_ERR_UNSUPPORTED;
+  const Layout L = make_layout(b);
+  if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
+  char* ws = (char*)workspace;
+  int rc = infcl::launch_bwd(img, txt, b, d, dtype, scale, lse_r, lse_c, aux, dloss, dimg, dtxt, dscale,
+                             (double*)(ws + L.bwd_part), (hipStream_t)stream);
+  if (rc == 2) return INFCL_ERR_UNSUPPORTED;
+  return rc == 0 ? INFCL_OK : INFCL_ERR_HIP;
+}
+
+const char* infcl_status_str(int status) {
+  switch (status) {
+    case INFCL_OK: return "ok";
+    case INFCL_ERR_INVALID: return "invalid argument (null or misaligned pointer, b < 1, d < 1 or unknown dtype)";
+    case INFCL_ERR_UNSUPPORTED: return "unsupported shape (bf16: d in 128..1024 step 128; f32: d in 64..512 step 64)";
+    case INFCL_ERR_WORKSPACE: return "workspace smaller than infcl_workspace_size()";
+    case INFCL_ERR_HIP: return "HIP kernel launch failed";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

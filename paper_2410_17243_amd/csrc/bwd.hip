@@ -1,0 +1,424 @@
+// Backward sweeps of the tiled symmetric InfoNCE loss (gfx950).
+//
+// What is computed (paper Sec. 3.1, Eq. 6-8, completed for both halves of the
+// symmetric loss, the text side and the scale; the appendix's in-GPU backward
+// algorithm recomputes every tile from the saved log-sum-exp vectors):
+//   dL/dx_ij = (1/2b) (P^r_ij + P^c_ij) - (1/b) delta_ij,
+//   P^r_ij = exp(x_ij - r_i),  P^c_ij = exp(x_ij - c_j),
+//   dimg = dloss * s * G img-side = k * G' txt,   dtxt = k * G'^T img,
+//   with G' = P^r + P^c off the diagonal, G'_ii = expm1(-(r_i-x_ii)) + expm1(-(c_i-x_ii)),
+//   k = dloss * s / (2b), and
+//   ds = dloss/(2b) * sum_{i != j} [P^r_ij (u_ij - u_ii) + P^c_ij (u_ij - u_jj)],  u = <img_i, txt_j>.
+//
+// Design (differs from the paper's single pass that read-modify-writes the text
+// gradient tile in HBM for every tile): one kernel template, launched twice.
+// The launch that "owns" the image rows keeps dimg rows in registers and sweeps
+// all text rows; the second launch swaps the roles (owns text rows, sweeps
+// image rows).  The similarity tile is recomputed in each launch, but no
+// gradient ever leaves the registers before the sweep ends and no atomics are
+// used.  Per tile and wave:
+//   GEMM1  S^T(32 swept x 32 own) = swept_tile * own^T   (own operand held in
+//          registers for the whole sweep, swept rows read from LDS with a
+//          row permutation that makes the accumulator usable as GEMM2's operand)
+//   G'     two exp2 per entry (log2 domain), the diagonal from expm1 terms
+//   GEMM2  dOwn(32 own x FP features) += G'(bf16) * swept_tile, the swept tile
+//          read feature-major through the transposing LDS read.
+// Feature widths whose accumulators do not fit the register file are split in
+// passes of FP features; each pass recomputes GEMM1.
+#include <type_traits>
+
+#include "common.hpp"
+
+namespace infcl {
+
+struct BwdParams {
+  const void* own;    // [b, d] rows whose gradient this launch produces
+  const void* swept;  // [b, d] the other modality
+  int64_t b, d;
+  const float* scale;
+  const float* lse_own;    // [b]
+  const float* lse_swept;  // [b]
+  const float* ell_own;    // [b]  r_i - x_ii of the own side
+  const float* ell_swept;  // [b]
+  const float* udiag;      // [b]  <img_i, txt_i>
+  const float* dloss;      // device scalar or nullptr (= 1)
+  float* dOwn;             // [b, d]
+  double* ds_part;         // [gridDim.x]
+};
+
+constexpr int kBwdBM = 128;  // own rows per workgroup (32 per wave)
+constexpr int kBwdBN = 32;   // swept rows per tile
+
+// Chunk swizzle for the swept tile (rows of >= 16 chunks): 16 rows reading one
+// logical chunk, and the 4 rows x 4 chunks of a transposing read, are both
+// spread over all 64 banks.
+__device__ __forceinline__ int bwd_g(int r) { return 4 * (r & 3) + ((r >> 2) & 3); }
+// GEMM1 row permutation: MFMA row m loads swept row perm(m) (bits 2 and 3
+// swapped), so that accumulator register 8s+t of lane half h holds swept row
+// 16s + 8h + t -- exactly the contraction slot t of GEMM2 step s.
+__device__ __forceinline__ int bwd_perm(int m) { return (m & 0x13) | ((m & 4) << 1) | ((m & 8) >> 1); }
+
+template <typename TIN, int D>
+__device__ __forceinline__ void bwd_tile_dma(const BwdParams& p, int64_t j0, INFCL_LDS char* buf, int wave,
+                                             int lane) {
+  constexpr int EPC = 16 / sizeof(TIN);
+  constexpr int CPR = D / EPC;               // chunks per row
+  constexpr int NI = kBwdBN * CPR / 64;      // DMA instructions per tile
+  static_assert(NI % 4 == 0, "tile DMA must split evenly over 4 waves");
+  const int64_t b = p.b;
+#pragma unroll
+  for (int kk = 0; kk < NI / 4; ++kk) {
+    const int k = wave + 4 * kk;
+    const int F = 64 * k + lane;
+    const int r = F / CPR, pc = F % CPR;
+    const int c = pc ^ bwd_g(r);
+    int64_t row = j0 + r;
+    row = row < b ? row : b - 1;
+    dma16((const TIN*)p.swept + row * D + c * EPC, (INFCL_LDS void*)(buf + 1024 * k));
+  }
+}
+
+template <typename TIN, int D, int FB>
+__global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
+  constexpr int ES = sizeof(TIN);
+  constexpr int KS = D / 16;            // 16-wide contraction steps of GEMM1
+  constexpr int CPR = D * ES / 16;      // 16-byte chunks per swept row
+  constexpr int ROWB = CPR * 16;        // bytes per swept row in LDS
+  constexpr int TILEB = kBwdBN * ROWB;  // bytes per swept tile
+  constexpr int FP = 32 * FB;           // features per pass
+  constexpr int NPASS = D / FP;
+  static_assert(D % FP == 0, "pass width must divide d");
+  static_assert(CPR % 16 == 0, "rows must hold a multiple of 16 chunks");
+  __shared__ __attribute__((aligned(1024))) char lds_[2 * TILEB];
+  INFCL_LDS char* lds = (INFCL_LDS char*)lds_;
+
+  const int lane = __lane_id();
+  const int wave = threadIdx.x >> 6;
+  const int l32 = lane & 31, h = lane >> 5;
+  const int64_t b = p.b;
+  const int64_t own0 = (int64_t)blockIdx.x * kBwdBM + 32 * wave;  // this wave's first own row
+  const int64_t iown = own0 + l32;                                // this lane's own row
+  const bool own_ok = iown < b;
+  const int64_t irow = own_ok ? iown : b - 1;
+  const bool wave_rows_ok = own0 + 32 <= b;
+
+  const float s = p.scale[0];
+  const float k2 = s * kLog2e;
+  const float dl = p.dloss ? p.dloss[0] : 1.0f;
+  const float kfin = dl * s / (2.0f * (float)b);
+
+  // own operand of GEMM1, held for the whole sweep: row irow, slots 8h..8h+7 of each step
+  typedef typename std::conditional<ES == 2, bf16x8, f32x4>::type frag_t;
+  constexpr int FR = ES == 2 ? 1 : 2;  // 16-byte loads per step and lane
+  frag_t ownf[KS][FR];
+  {
+    const char* src = (const char*)p.own + (irow * D) * ES;
+#pragma unroll
+    for (int s2 = 0; s2 < KS; ++s2)
+#pragma unroll
+      for (int u = 0; u < FR; ++u) ownf[s2][u] = *(const frag_t*)(src + (16 * s2 + 8 * h) * ES + 16 * u);
+  }
+  const float aO = own_ok ? p.lse_own[iown] * kLog2e : 0.f;
+  const float uO = own_ok ? p.udiag[iown] : 0.f;
+  const float gdiag = own_ok ? expm1f(-p.ell_own[iown]) + expm1f(-p.ell_swept[iown]) : 0.f;
+
+  // ---- per-lane LDS offsets; every read below is one of these plus an immediate
+  // GEMM1 (row-fragment) reads: swept row perm(l32), logical chunk 16*s_hi + cl,
+  // physical chunk 16*s_hi + (cl ^ g(row)).
+  constexpr int NA = ES == 2 ? 8 : 8;  // distinct cl patterns
+  int offA[NA];
+  {
+    const int rA = bwd_perm(l32);
+    const int gA = bwd_g(rA);
+#pragma unroll
+    for (int k = 0; k < NA; ++k) {
+      const int cl = ES == 2 ? (2 * k + h) : (4 * (k >> 1) + 2 * h + (k & 1));
+      offA[k] = rA * ROWB + 16 * (cl ^ gA);
+    }
+  }
+  // GEMM2 transposing reads: row 16 s2 + 4 t + (8 hh + e), feature 32 fbabs + 16 nb16 + 4 qq
+  // -> physical chunk 16 (fbabs >> 2) + 4 ((fbabs & 3) ^ e) + (lo ^ ((t + 2 hh) & 3)).
+  int offT[2][4];
+  {
+    const int g4 = lane >> 4, l16 = lane & 15;
+    const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
+    const int lo = 2 * nb16 + (qq >> 1);
+    const int fo = (qq & 1) * 8;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int fm = 0; fm < 4; ++fm)
+        offT[t][fm] = (8 * hh + e) * ROWB + 16 * (4 * (fm ^ e) + (lo ^ ((t + 2 * hh) & 3))) + fo;
+  }
+  // fp32 GEMM2 reads: swept row jr(r, h), feature 32 fbabs + l32 -> chunk 8 fbabs + (l32 >> 2)
+  int offF[16];
+  if constexpr (ES == 4) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int j = bwd_perm(8 * (r >> 2) + 4 * h + (r & 3));
+      offF[r] = j * ROWB + (l32 & 3) * 4;  // chunk part added per feature block below
+    }
+  }
+
+  double ds_acc = 0.0;
+  const int ntile = (int)((b + kBwdBN - 1) / kBwdBN);
+
+  for (int pass = 0; pass < NPASS; ++pass) {
+    f32x16 dacc[FB];
+#pragma unroll
+    for (int fb = 0; fb < FB; ++fb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dacc[fb][r] = 0.f;
+
+    bwd_tile_dma<TIN, D>(p, 0, lds, wave, lane);
+    wait_dma();
+    __syncthreads();
+
+    for (int jt = 0; jt < ntile; ++jt) {
+      const int cur_off = (jt & 1) * TILEB;
+      const INFCL_LDS char* cur = lds + cur_off;
+      if (jt + 1 < ntile) bwd_tile_dma<TIN, D>(p, (int64_t)(jt + 1) * kBwdBN, lds + (TILEB - cur_off), wave, lane);
+      const int64_t j0 = (int64_t)jt * kBwdBN;
+
+      // ---- GEMM1: S^T block, MFMA row m <-> swept row j0 + perm(m)
+      f32x16 sacc;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[r] = 0.f;
+      if constexpr (ES == 2) {
+#pragma unroll
+        for (int s2 = 0; s2 < KS; ++s2) {
+          bf16x8 a = *(const INFCL_LDS bf16x8*)(cur + offA[s2 & 7] + 256 * (s2 >> 3));
+          sacc = mfma_bf16(a, ownf[s2][0], sacc);
+        }
+      } else {
+#pragma unroll
+        for (int s2 = 0; s2 < KS; ++s2) {
+          const int kb = 2 * (s2 & 3);
+          f32x4 a0 = *(const INFCL_LDS f32x4*)(cur + offA[kb] + 256 * (s2 >> 2));
+          f32x4 a1 = *(const INFCL_LDS f32x4*)(cur + offA[kb + 1] + 256 * (s2 >> 2));
+#pragma unroll
+          for (int t = 0; t < 4; ++t) sacc = mfma_f32(a0[t], ownf[s2][0][t], sacc);
+#pragma unroll
+          for (int t = 0; t < 4; ++t) sacc = mfma_f32(a1[t], ownf[s2][1][t], sacc);
+        }
+      }
+
+      // ---- G' (log2 domain): entry r <-> swept row j = j0 + 16 (r>>3) + 8h + (r&7)
+      float gv[16];
+      float ds_tile = 0.f;
+      const bool special = (j0 == own0) || (j0 + kBwdBN > b) || !wave_rows_ok;
+      if (!special) {
+        float aS[16];
+#pragma unroll
+        for (int a4 = 0; a4 < 4; ++a4) {
+          f32x4 v = *(const f32x4*)(p.lse_swept + j0 + 16 * (a4 >> 1) + 8 * h + 4 * (a4 & 1));
+#pragma unroll
+          for (int c = 0; c < 4; ++c) aS[4 * a4 + c] = v[c] * kLog2e;
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float pO = exp2_hw(__builtin_fmaf(sacc[r], k2, -aO));
+          const float pS = exp2_hw(__builtin_fmaf(sacc[r], k2, -aS[r]));
+          gv[r] = pO + pS;
+          ds_tile = __builtin_fmaf(pO, sacc[r] - uO, ds_tile);
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int64_t j = j0 + 16 * (r >> 3) + 8 * h + (r & 7);
+          const bool jok = j < b;
+          const float aSr = p.lse_swept[jok ? j : b - 1] * kLog2e;
+          const float pO = exp2_hw(__builtin_fmaf(sacc[r], k2, -aO));
+          const float pS = exp2_hw(__builtin_fmaf(sacc[r], k2, -aSr));
+          const bool ok = own_ok && jok;
+          const bool dg = (j == iown);
+          float gg = ok ? pO + pS : 0.f;
+          gg = dg ? gdiag : gg;
+          gv[r] = gg;
+          ds_tile += (ok && !dg) ? pO * (sacc[r] - uO) : 0.f;
+        }
+      }
+      if (pass == 0) ds_acc += (double)ds_tile;
+
+      // ---- GEMM2: dOwn(own rows x pass features) += G' * swept_tile
+      if constexpr (ES == 2) {
+        bf16x8 ga[2];
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+          for (int t = 0; t < 8; ++t) ga[s2][t] = (__bf16)gv[8 * s2 + t];
+        // FB is a multiple of 4, so feature block pass*FB+fb has low bits fb&3 and
+        // its chunk group (>> 2) splits into a per-pass base and an immediate.
+        const INFCL_LDS char* curT = cur + 64 * FB * pass;
+#pragma unroll
+        for (int fb = 0; fb < FB; ++fb) {
+#pragma unroll
+          for (int s2 = 0; s2 < 2; ++s2) {
+            const int imm = 16 * s2 * ROWB + 256 * (fb >> 2);
+            s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (INFCL_LDS s16x4*)(curT + offT[0][fb & 3] + imm));
+            s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (INFCL_LDS s16x4*)(curT + offT[1][fb & 3] + 4 * ROWB + imm));
+            typedef short s16x8 __attribute__((ext_vector_type(8)));
+            s16x8 bb = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            dacc[fb] = mfma_bf16(ga[s2], __builtin_bit_cast(bf16x8, bb), dacc[fb]);
+          }
+        }
+      } else {
+        // fp32: step r contracts swept row jr(r, h) of each lane half
+#pragma unroll
+        for (int fb = 0; fb < FB; ++fb) {
+          const int fbabs = pass * FB + fb;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int j = bwd_perm(8 * (r >> 2) + 4 * h + (r & 3));
+            const int cf = 8 * fbabs + (l32 >> 2);
+            float bv = *(const INFCL_LDS float*)(cur + offF[r] + 16 * (cf ^ bwd_g(j)));
+            dacc[fb] = mfma_f32(gv[r], bv, dacc[fb]);
+          }
+        }
+      }
+
+      wait_dma();
+      __syncthreads();
+    }
+
+    // ---- write dOwn rows of this pass: lane holds feature l32 of block fb, rows 8(r>>2)+4h+(r&3)
+    float* dst = p.dOwn + (own0 + 4 * h) * D + 32 * pass * FB + l32;
+    if (wave_rows_ok) {
+#pragma unroll
+      for (int fb = 0; fb < FB; ++fb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fb] = kfin * dacc[fb][r];
+    } else {
+#pragma unroll
+      for (int fb = 0; fb < FB; ++fb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int64_t row = own0 + 8 * (r >> 2) + 4 * h + (r & 3);
+          if (row < b) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fb] = kfin * dacc[fb][r];
+        }
+    }
+  }
+
+  // ---- dscale partial of this workgroup: fixed-order reduction
+  __shared__ double red[256];
+  red[threadIdx.x] = ds_acc;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) p.ds_part[blockIdx.x] = red[0];
+}
+
+// dscale = dloss / (2b) * (sum of both launches' partials), fixed order
+__global__ void __launch_bounds__(256) dscale_finish(const double* part, int64_t n, int64_t b, const float* dloss,
+                                                     float* dscale) {
+  __shared__ double red[256];
+  double s = 0.0;
+  for (int64_t k = threadIdx.x; k < n; k += 256) s += part[k];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const double dl = dloss ? (double)dloss[0] : 1.0;
+    *dscale = (float)(red[0] * dl / (2.0 * (double)b));
+  }
+}
+
+// Pass width: largest FB (32-feature blocks) dividing d/32 whose accumulators
+// (16 FB registers) fit next to the own operand (d/4 or d/2 registers); for
+// bf16 FB is also a multiple of 4 (see the transposing-read addressing).
+template <typename TIN, int D>
+static int launch_bwd_d(const BwdParams& p, int nwg, hipStream_t stream) {
+  constexpr int ES = sizeof(TIN);
+  constexpr int OWNREGS = D * ES / 8;
+  constexpr int NB32 = D / 32;
+  constexpr int FBMAX = (384 - OWNREGS) / 16;
+  constexpr int FB = [] {
+    int best = 1;
+    for (int f = 1; f <= NB32; ++f)
+      if (NB32 % f == 0 && f <= FBMAX && (ES == 4 || f % 4 == 0)) best = f;
+    return best;
+  }();
+  static_assert(ES == 4 || FB % 4 == 0, "bf16 pass width must be a multiple of 128 features");
+  hipLaunchKernelGGL((bwd_sweep<TIN, D, FB>), dim3(nwg), dim3(256), 0, stream, p);
+  return hipGetLastError() == hipSuccess ? 0 : 1;
+}
+
+template <typename TIN>
+static int launch_bwd_t(const BwdParams& p, int nwg, hipStream_t stream) {
+  const int64_t d = p.d;
+  if constexpr (sizeof(TIN) == 2) {
+    switch (d) {
+      case 128: return launch_bwd_d<TIN, 128>(p, nwg, stream);
+      case 256: return launch_bwd_d<TIN, 256>(p, nwg, stream);
+      case 384: return launch_bwd_d<TIN, 384>(p, nwg, stream);
+      case 512: return launch_bwd_d<TIN, 512>(p, nwg, stream);
+      case 640: return launch_bwd_d<TIN, 640>(p, nwg, stream);
+      case 768: return launch_bwd_d<TIN, 768>(p, nwg, stream);
+      case 896: return launch_bwd_d<TIN, 896>(p, nwg, stream);
+      case 1024: return launch_bwd_d<TIN, 1024>(p, nwg, stream);
+    }
+  } else {
+    switch (d) {
+      case 64: return launch_bwd_d<TIN, 64>(p, nwg, stream);
+      case 128: return launch_bwd_d<TIN, 128>(p, nwg, stream);
+      case 192: return launch_bwd_d<TIN, 192>(p, nwg, stream);
+      case 256: return launch_bwd_d<TIN, 256>(p, nwg, stream);
+      case 320: return launch_bwd_d<TIN, 320>(p, nwg, stream);
+      case 384: return launch_bwd_d<TIN, 384>(p, nwg, stream);
+      case 448: return launch_bwd_d<TIN, 448>(p, nwg, stream);
+      case 512: return launch_bwd_d<TIN, 512>(p, nwg, stream);
+    }
+  }
+  return 2;
+}
+
+int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale,
+               const float* lse_r, const float* lse_c, const float* aux, const float* dloss, float* dimg, float* dtxt,
+               float* dscale, double* ds_part, hipStream_t stream) {
+  const int nwg = (int)((b + kBwdBM - 1) / kBwdBM);
+  BwdParams p;
+  p.b = b;
+  p.d = d;
+  p.scale = scale;
+  p.udiag = aux + 2 * b;
+  p.dloss = dloss;
+  // launch 1: own = image rows (dimg), swept = text rows
+  p.own = img;
+  p.swept = txt;
+  p.lse_own = lse_r;
+  p.lse_swept = lse_c;
+  p.ell_own = aux;
+  p.ell_swept = aux + b;
+  p.dOwn = dimg;
+  p.ds_part = ds_part;
+  int rc = dtype == 0 ? launch_bwd_t<__bf16>(p, nwg, stream) : launch_bwd_t<float>(p, nwg, stream);
+  if (rc) return rc;
+  // launch 2: own = text rows (dtxt), swept = image rows
+  p.own = txt;
+  p.swept = img;
+  p.lse_own = lse_c;
+  p.lse_swept = lse_r;
+  p.ell_own = aux + b;
+  p.ell_swept = aux;
+  p.dOwn = dtxt;
+  p.ds_part = ds_part + nwg;
+  rc = dtype == 0 ? launch_bwd_t<__bf16>(p, nwg, stream) : launch_bwd_t<float>(p, nwg, stream);
+  if (rc) return rc;
+  hipLaunchKernelGGL(dscale_finish, dim3(1), dim3(256), 0, stream, (const double*)ds_part, (int64_t)2 * nwg, b,
+                     dloss, dscale);
+  return hipGetLastError() == hipSuccess ? 0 : 1;
+}
+
+bool bwd_supported(int64_t d, int dtype) {
+  if (dtype == 0) return d % 128 == 0 && d >= 128 && d <= 1024;
+  return d % 64 == 0 && d >= 64 && d <= 512;
+}
+
+}  // namespace infcl

@@ -1,0 +1,73 @@
+// Shared device helpers for the tiled contrastive-loss kernels (gfx950 only).
+//
+// Conventions used by both sweeps
+//   - Matrix products run on the 32x32x16 bf16 MFMA (fp32 accumulate) or the
+//     32x32x2 fp32 MFMA.  For a 32x32 output block, lane L holds column
+//     n = L % 32 and rows m = 8*(r/4) + 4*(L/32) + r%4 for accumulator r = 0..15.
+//     Operand fragments: lane L holds row L % 32 and the 8 consecutive
+//     contraction slots 8*(L/32) .. 8*(L/32)+7 of a 16-wide contraction step.
+//   - Log-sum-exp statistics are kept in base 2: y = s*log2(e)*<a, b>, a
+//     running pair (R, l) stands for log2(l) + R, and exp2 maps to v_exp_f32.
+//   - Tiles are staged in LDS in 16-byte chunks with an XOR swizzle of the chunk
+//     index so that both the row-fragment reads and the transposing reads of
+//     the backward pass are bank-conflict free.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace infcl {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+#define INFCL_LDS __attribute__((address_space(3)))
+#define INFCL_GLOBAL __attribute__((address_space(1)))
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+// A per-tile partial sum above this bound, or a non-finite one, sends a tile
+// through the exact (max-rescaled) path.  With at most 2^22 terms per sum the
+// accumulated value stays below 2^86, far from float overflow.
+constexpr float kLazyBound = 18446744073709551616.0f;  // 2^64
+
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ f32x16 mfma_bf16(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x16 mfma_f32(float a, float b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+
+// Asynchronous 16-byte global -> LDS copy.  Lane L writes LDS bytes
+// [lds_base + 16 L, lds_base + 16 L + 16); lds_base must be wave-uniform.
+__device__ __forceinline__ void dma16(const void* gsrc, INFCL_LDS void* lds_base) {
+  __builtin_amdgcn_global_load_lds((const INFCL_GLOBAL void*)gsrc, lds_base, 16, 0, 0);
+}
+__device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Merge of two base-2 log-sum-exp pairs (R, l) -> (max R, rescaled sum).
+__device__ __forceinline__ void lse2_merge(float& R, float& l, float R2, float l2) {
+  float M = fmaxf(R, R2);
+  if (M == -__builtin_inff()) return;  // both empty
+  l = l * exp2_hw(R - M) + l2 * exp2_hw(R2 - M);
+  R = M;
+}
+
+__device__ __forceinline__ bool lazy_ok(float t) { return t <= kLazyBound; }  // false for NaN/inf
+
+// Cross-lane helpers (full 64-lane wave).
+__device__ __forceinline__ float shfl_xor(float v, int mask) {
+  int l = __lane_id();
+  return __int_as_float(__builtin_amdgcn_ds_bpermute((l ^ mask) << 2, __float_as_int(v)));
+}
+__device__ __forceinline__ float shfl_idx(float v, int src) {
+  return __int_as_float(__builtin_amdgcn_ds_bpermute(src << 2, __float_as_int(v)));
+}
+__device__ __forceinline__ bool wave_any(bool p) { return __builtin_amdgcn_ballot_w64(p) != 0; }
+
+}  // namespace infcl

@@ -1,0 +1,91 @@
+"""C ABI checks that need no GPU: the library loads, exports every function the
+header declares, and rejects invalid arguments on the host before launching."""
+
+import ctypes
+
+import pytest
+
+import paper_2410_17243_amd as infcl
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return infcl.load_library()
+
+
+def test_exports_every_declared_function(lib):
+    names = infcl.header_functions()
+    assert set(names) == {"infcl_workspace_size", "infcl_fwd", "infcl_bwd", "infcl_status_str"}
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    for st in range(5):
+        assert isinstance(infcl.status_str(st), str) and infcl.status_str(st)
+    assert infcl.status_str(99) == "unknown status"
+
+
+def _ws(b, d, dt):
+    out = ctypes.c_size_t(0)
+    st = infcl.load_library().infcl_workspace_size(b, d, dt, ctypes.byref(out))
+    return st, out.value
+
+
+def test_workspace_size_is_linear_in_b():
+    st1, w1 = _ws(1 << 20, 768, infcl.INFCL_BF16)
+    st2, w2 = _ws(1 << 21, 768, infcl.INFCL_BF16)
+    assert st1 == st2 == infcl.INFCL_OK
+    assert 0 < w1 < 1024 * (1 << 20)         # under 1 KiB per sample
+    assert abs(w2 - 2 * w1) < 1 << 16        # linear in b (up to alignment)
+    assert _ws(1, 128, infcl.INFCL_BF16)[0] == infcl.INFCL_OK
+
+
+@pytest.mark.parametrize("b,d,dt,expect", [
+    (0, 512, 0, infcl.INFCL_ERR_INVALID), (-3, 512, 0, infcl.INFCL_ERR_INVALID), (16, 0, 0, infcl.INFCL_ERR_INVALID),
+    (16, 512, 7, infcl.INFCL_ERR_INVALID), (16, 100, 0, infcl.INFCL_ERR_UNSUPPORTED),
+    (16, 2048, 0, infcl.INFCL_ERR_UNSUPPORTED), (16, 1024, 1, infcl.INFCL_ERR_UNSUPPORTED),
+    (16, 64, 0, infcl.INFCL_ERR_UNSUPPORTED), (16, 64, 1, infcl.INFCL_OK), ((1 << 30) + 1, 512, 0, infcl.INFCL_ERR_UNSUPPORTED),
+])
+def test_workspace_size_validation(b, d, dt, expect):
+    assert _ws(b, d, dt)[0] == expect
+
+
+def test_workspace_size_null_out(lib):
+    assert lib.infcl_workspace_size(16, 512, 0, None) == infcl.INFCL_ERR_INVALID
+
+
+# Fake but aligned device addresses: every call below must return before any launch.
+A = 1 << 20
+
+
+def _fwd(lib, img=A, txt=A, b=64, d=512, dt=0, scale=A, loss=A, loss64=A, lr=A, lc=A, aux=A, ws=A, wsb=1 << 30):
+    return lib.infcl_fwd(img, txt, b, d, dt, scale, loss, loss64, lr, lc, aux, ws, wsb, None)
+
+
+def _bwd(lib, img=A, txt=A, b=64, d=512, dt=0, scale=A, lr=A, lc=A, aux=A, dloss=A, di=A, dtx=A, ds=A, ws=A,
+         wsb=1 << 30):
+    return lib.infcl_bwd(img, txt, b, d, dt, scale, lr, lc, aux, dloss, di, dtx, ds, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(img=None), infcl.INFCL_ERR_INVALID), (dict(txt=A + 8), infcl.INFCL_ERR_INVALID),
+    (dict(scale=None), infcl.INFCL_ERR_INVALID), (dict(loss=None), infcl.INFCL_ERR_INVALID),
+    (dict(loss64=A + 4), infcl.INFCL_ERR_INVALID), (dict(lr=A + 4), infcl.INFCL_ERR_INVALID),
+    (dict(aux=None), infcl.INFCL_ERR_INVALID), (dict(ws=A + 16), infcl.INFCL_ERR_INVALID),
+    (dict(b=0), infcl.INFCL_ERR_INVALID), (dict(d=-1), infcl.INFCL_ERR_INVALID), (dict(dt=3), infcl.INFCL_ERR_INVALID),
+    (dict(d=96), infcl.INFCL_ERR_UNSUPPORTED), (dict(wsb=16), infcl.INFCL_ERR_WORKSPACE),
+])
+def test_fwd_validation(lib, kw, expect):
+    assert _fwd(lib, **kw) == expect
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(di=None), infcl.INFCL_ERR_INVALID), (dict(dtx=A + 4), infcl.INFCL_ERR_INVALID),
+    (dict(ds=None), infcl.INFCL_ERR_INVALID), (dict(dloss=A + 2), infcl.INFCL_ERR_INVALID),
+    (dict(lc=None), infcl.INFCL_ERR_INVALID), (dict(b=-5), infcl.INFCL_ERR_INVALID),
+    (dict(d=1536), infcl.INFCL_ERR_UNSUPPORTED), (dict(dt=1, d=768), infcl.INFCL_ERR_UNSUPPORTED),
+    (dict(wsb=0), infcl.INFCL_ERR_WORKSPACE),
+])
+def test_bwd_validation(lib, kw, expect):
+    assert _bwd(lib, **kw) == expect

@@ -1,0 +1,70 @@
+"""Parity at the benchmark's full sizes, in the launch configuration bench.py
+times, on outputs the oracle can compute one by one.
+
+For b = 32768 (d = 512, s = 14.29) and b = 131072 (d = 768, s = 100) the
+full oracle takes minutes to hours, so:
+  * r_i, r_i - x_ii for 96 seeded rows and c_j, c_j - x_jj for 96 seeded
+    columns come from the exact sampled oracle (independent of the GPU);
+  * dimg rows / dtxt rows for the same indices are recomputed in fp64 from the
+    inputs, the oracle's own log-sum-exp of that row and the GPU's log-sum-exp
+    of the other side (semi-independent: the other side's values are checked
+    only on the sampled indices);
+  * <dimg, img> = <dtxt, txt> = s * dscale must hold for the whole batch.
+"""
+
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import f32_scale, lse_tol, max_rel, run, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _grad_rows(A, B, s, rows, lse_own_rows, lse_other_all, ell_own_rows, ell_other_rows, b):
+    """fp64 rows of dOwn = k * G' Other for own rows `rows` (own = A, other = B)."""
+    k = s / (2.0 * b)
+    x = s * (A[rows] @ B.T)
+    g = np.exp(x - lse_own_rows[:, None]) + np.exp(x - lse_other_all[None, :])
+    g[np.arange(len(rows)), rows] = np.expm1(-ell_own_rows) + np.expm1(-ell_other_rows)
+    return k * (g @ B)
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_full_size_sampled(cfg):
+    c = synth.CONFIGS[cfg]
+    b, d, s = c["b"], c["d"], f32_scale(c["scale"])
+    img, txt = synth.clip_pairs(b, d, c["sigma"], seed=0, dtype="bf16")
+    g = run(img, txt, "bf16", s)
+    I = synth.as_f64(img, "bf16")
+    T = synth.as_f64(txt, "bf16")
+    rows = np.sort(np.random.default_rng(1234).choice(b, size=96, replace=False))
+    rows[0], rows[-1] = 0, b - 1
+    sr = oracle.sampled_rows(I, T, s, rows)
+    sc = oracle.sampled_cols(I, T, s, rows)
+    err_r = np.max(np.abs(g["lse_r"][rows] - sr["lse"]))
+    err_c = np.max(np.abs(g["lse_c"][rows] - sc["lse"]))
+    print(f"config {cfg}: loss {g['loss64']:.6e}; lse_r err {err_r:.2e} lse_c err {err_c:.2e}", flush=True)
+    assert np.all(np.abs(g["lse_r"][rows] - sr["lse"]) <= lse_tol(s, d, sr["lse"]))
+    assert np.all(np.abs(g["lse_c"][rows] - sc["lse"]) <= lse_tol(s, d, sc["lse"]))
+    # per-sample terms: relative accuracy of r_i - x_ii (cancellation-free on both sides)
+    rel_r = np.abs(g["ell_r"][rows] - sr["ell"]) / np.maximum(sr["ell"], 1e-300)
+    rel_c = np.abs(g["ell_c"][rows] - sc["ell"]) / np.maximum(sc["ell"], 1e-300)
+    print(f"  ell rel err rows {np.max(rel_r):.2e} cols {np.max(rel_c):.2e}", flush=True)
+    assert np.max(rel_r) <= 2e-2 and np.max(rel_c) <= 2e-2
+    # the loss is the mean of the per-sample terms the GPU exported
+    assert g["loss64"] == pytest.approx((math.fsum(g["ell_r"]) + math.fsum(g["ell_c"])) / (2 * b), rel=1e-6)
+    # gradient rows
+    dI_ref = _grad_rows(I, T, s, rows, sr["lse"], g["lse_c"], sr["ell"], g["ell_c"][rows], b)
+    dT_ref = _grad_rows(T, I, s, rows, sc["lse"], g["lse_r"], sc["ell"], g["ell_r"][rows], b)
+    e1, e2 = max_rel(g["dI"][rows], dI_ref), max_rel(g["dT"][rows], dT_ref)
+    print(f"  dI rows {e1:.2e} dT rows {e2:.2e}", flush=True)
+    assert e1 <= 2e-2 and e2 <= 2e-2
+    # whole-batch invariant
+    a1 = math.fsum((g["dI"] * I).sum(axis=1))
+    a2 = math.fsum((g["dT"] * T).sum(axis=1))
+    print(f"  <dI,I> {a1:.6e} <dT,T> {a2:.6e} s*dscale {s * g['dscale']:.6e}", flush=True)
+    assert a1 == pytest.approx(s * g["dscale"], rel=2e-2, abs=1e-30)
+    assert a2 == pytest.approx(s * g["dscale"], rel=2e-2, abs=1e-30)

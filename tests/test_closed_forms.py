@@ -1,0 +1,111 @@
+"""GPU path vs closed forms that hold at any size (inputs exact in bf16).
+
+A: identical embeddings: every x_ij = s, so r_i = c_j = s + log b and L = log b.
+B: one-hot pairs I_i = T_i = e_i (d >= b): L = log1p((b-1) e^{-s}), exact even
+   where L is far below the float range (s = 100); dscale = -(b-1)/(e^s + b - 1).
+C: periodic one-hot I_i = T_i = e_{i mod d} (b > d): with n_i the size of i's
+   class, r_i = c_i = log(n_i e^s + b - n_i), and the gradients have per-class
+   closed forms; this covers the full path (all tiles, partial merges, ragged
+   ends) at the benchmark shapes.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import f32_scale, lse_tol, max_rel, run
+
+pytestmark = pytest.mark.gpu
+
+
+def _onehot(b, d, period):
+    I = np.zeros((b, d), dtype=np.uint16)
+    I[np.arange(b), np.arange(b) % period] = 0x3F80  # bf16 1.0
+    return I
+
+
+@pytest.mark.parametrize("b,s", [(1000, 14.29), (4097, 100.0), (32768, 14.29)])
+def test_A_identical(b, s):
+    d = 128
+    I = np.zeros((b, d), dtype=np.uint16)
+    I[:, 5] = 0x3F80
+    g = run(I, I.copy(), "bf16", f32_scale(s))
+    assert g["loss64"] == pytest.approx(math.log(b), rel=1e-6)
+    np.testing.assert_allclose(g["lse_r"], f32_scale(s) + math.log(b), rtol=1e-6)
+    np.testing.assert_allclose(g["lse_c"], f32_scale(s) + math.log(b), rtol=1e-6)
+    # exact gradient is 0; what remains is bf16 rounding of G' = 2/b, summed over a row
+    k = f32_scale(s) / (2 * b)
+    assert np.max(np.abs(g["dI"])) <= 2 * k * 2.0 ** -8 * 2
+    assert abs(g["dscale"]) <= 1e-6
+
+
+def _closed_B(b, s):
+    Z = math.exp(s) + b - 1
+    return math.log1p((b - 1) * math.exp(-s)), math.log(Z), -(b - 1) / Z, (s / b) * (-(b - 1) / Z), (s / b) / Z
+
+
+@pytest.mark.parametrize("b,d,s", [(128, 128, 100.0), (100, 128, 14.29), (512, 512, 50.0), (1000, 1024, 100.0)])
+def test_B_one_hot_pairs(b, d, s):
+    s32 = f32_scale(s)
+    I = _onehot(b, d, d)
+    g = run(I, I.copy(), "bf16", s32)
+    loss, lse, ds, gdiag, goff = _closed_B(b, s32)
+    assert g["loss64"] == pytest.approx(loss, rel=1e-3)
+    np.testing.assert_allclose(g["lse_r"], lse, rtol=1e-6)
+    np.testing.assert_allclose(g["lse_c"], lse, rtol=1e-6)
+    if s <= 20:  # at larger s the exact gradients are below the float range
+        assert abs(g["dscale"] - ds) <= 2e-2 * abs(ds) + 2.0 ** -120
+        ref = np.full((b, b), goff)
+        np.fill_diagonal(ref, gdiag)
+        assert max_rel(g["dI"][:, :b], ref) <= 2e-2
+        assert max_rel(g["dT"][:, :b], ref) <= 2e-2
+
+
+def _closed_C(b, d, s):
+    """Closed forms for periodic one-hot inputs, plus the per-element error
+    bound of the GPU's arithmetic: bf16 rounding of every G' term (relative
+    2^-9) in the second product, and float exponentials that flush results
+    below 2^-126 to zero:  bound[i, f] = (s/2b) (2^-9 sum_j |G'_ij| |T_jf| + 2^-120)."""
+    cls = np.arange(b) % d
+    n = np.bincount(cls, minlength=d).astype(np.float64)
+    es = math.exp(s)
+    Zc = n * es + (b - n)
+    r = np.log(Zc)[cls]
+    ell = np.log(n + (b - n) * math.exp(-s))           # r_i - s per class
+    loss = math.fsum(r - s) / b
+    coef = np.zeros((d, d))   # coef[class of i][class kappa]
+    absg = np.zeros((d, d))   # sum_j |G'_ij| over j in class kappa (before the s/2b factor)
+    for c in range(d):
+        row = n * (1.0 / Zc[c] + 1.0 / Zc) / (2 * b)
+        row[c] = -(b - n[c]) / (b * Zc[c])      # n e^s / (b Z) - 1/b without cancellation
+        coef[c] = s * row
+        a = n * (1.0 / Zc[c] + 1.0 / Zc)
+        a[c] = (n[c] - 1) * 2 * es / Zc[c] + abs(2 * math.expm1(-ell[c]))
+        absg[c] = a
+    ds = -(1.0 / b) * math.fsum((b - n[cls]) / Zc[cls])
+    bound = (s / (2 * b)) * (2.0 ** -9 * absg[cls] + 2.0 ** -120)
+    return loss, r, coef[cls], ds, bound
+
+
+@pytest.mark.parametrize("b,d,s", [(32768, 512, 14.29), (131072, 768, 100.0), (5000, 128, 50.0), (33000, 256, 14.29)])
+def test_C_periodic_one_hot(b, d, s):
+    s32 = f32_scale(s)
+    I = _onehot(b, d, d)
+    g = run(I, I.copy(), "bf16", s32)
+    loss, r, dI, ds, bound = _closed_C(b, d, s32)
+    excess_I = np.max(np.abs(g["dI"] - dI) / (bound + 1e-3 * np.max(np.abs(dI))))
+    excess_T = np.max(np.abs(g["dT"] - dI) / (bound + 1e-3 * np.max(np.abs(dI))))
+    # at s = 100 the exact gradients (~1e-44) are below the float range: the
+    # check then reduces to "within the rounding bound of zero"
+    print(f"C b={b} d={d} s={s}: loss {g['loss64']:.9e} vs {loss:.9e}, dI err/bound {excess_I:.2e}, "
+          f"dT err/bound {excess_T:.2e}, ds {g['dscale']:.6e} vs {ds:.6e}", flush=True)
+    assert g["loss64"] == pytest.approx(loss, rel=1e-4)
+    assert np.all(np.abs(g["lse_r"] - r) <= lse_tol(s32, d, r))
+    assert np.all(np.abs(g["lse_c"] - r) <= lse_tol(s32, d, r))
+    # Identical embeddings make the own-class gradient a difference of nearly
+    # equal sums, so the bar is the bf16 rounding bound of G', element by element
+    # (plus 1e-3 of the largest entry for the fp32 exponentials and accumulation).
+    assert excess_I <= 1.0 and excess_T <= 1.0
+    assert abs(g["dscale"] - ds) <= 2e-2 * abs(ds) + 2.0 ** -120

@@ -1,0 +1,98 @@
+"""GPU path vs the fp64 oracle, element by element, on seeded synthetic inputs.
+
+Bars (bf16 embeddings, fp32 accumulation): loss relative error <= 1e-3;
+gradients max|diff| / max|ref| <= 2e-2; dscale relative <= 2e-2; the row and
+column log-sum-exp within the fp32-accumulation bound of gpu_util.lse_tol.
+fp32 embeddings: loss <= 1e-5 relative, gradients <= 1e-4 (the G' operand of
+the second product stays fp32 there).
+"""
+
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import f32_scale, lse_tol, max_rel, run, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _check(gpu, ref, dI, dT, ds, s, d, dtype, loss_tol=None, grad_tol=None):
+    loss_tol = loss_tol or (1e-3 if dtype == "bf16" else 1e-5)
+    grad_tol = grad_tol or (2e-2 if dtype == "bf16" else 1e-4)
+    print(f"loss gpu {gpu['loss64']:.9e} ref {ref['loss']:.9e} | lse_r err {np.max(np.abs(gpu['lse_r'] - ref['lse_r'])):.2e}"
+          f" lse_c err {np.max(np.abs(gpu['lse_c'] - ref['lse_c'])):.2e} | dI {max_rel(gpu['dI'], dI):.2e}"
+          f" dT {max_rel(gpu['dT'], dT):.2e} | ds gpu {gpu['dscale']:.6e} ref {ds:.6e}", flush=True)
+    assert gpu["loss64"] == pytest.approx(ref["loss"], rel=loss_tol, abs=1e-30)
+    assert gpu["loss"] == pytest.approx(ref["loss"], rel=max(loss_tol, 2e-7), abs=1e-37)
+    tol = lse_tol(s, d, ref["lse_r"])
+    assert np.all(np.abs(gpu["lse_r"] - ref["lse_r"]) <= tol)
+    assert np.all(np.abs(gpu["lse_c"] - ref["lse_c"]) <= lse_tol(s, d, ref["lse_c"]))
+    assert np.all(gpu["ell_r"] >= 0) and np.all(gpu["ell_c"] >= 0)
+    assert max_rel(gpu["dI"], dI) <= grad_tol
+    assert max_rel(gpu["dT"], dT) <= grad_tol
+    scale_g = max(np.max(np.abs(dI)), np.max(np.abs(dT)), 1e-30)
+    assert abs(gpu["dscale"] - ds) <= grad_tol * abs(ds) + 1e-6 * scale_g
+
+
+def _case(b, d, s, sigma=1.0, dtype="bf16", seed=0, mode="clip", dloss=1.0):
+    img, txt = synth.clip_pairs(b, d, sigma, seed=seed, dtype=dtype, mode=mode)
+    I = synth.as_f64(img, dtype)
+    T = synth.as_f64(txt, dtype)
+    s32 = f32_scale(s)
+    fwd, dI, dT, ds = oracle.forward_backward(I, T, s32, dloss=dloss)
+    gpu = run(img, txt, dtype, s32, dloss=dloss)
+    return gpu, fwd, dI, dT, ds, s32
+
+
+@pytest.mark.parametrize("b", [1, 2, 3, 17, 64, 65, 255, 256, 257, 1000, 1023, 1025, 2048])
+def test_ragged_batch_bf16(b):
+    gpu, fwd, dI, dT, ds, s = _case(b, 128, 14.29, seed=b)
+    _check(gpu, fwd, dI, dT, ds, s, 128, "bf16")
+
+
+@pytest.mark.parametrize("d", [256, 384, 512, 640, 768, 896, 1024])
+def test_feature_widths_bf16(d):
+    gpu, fwd, dI, dT, ds, s = _case(777, d, 14.29, seed=d)
+    _check(gpu, fwd, dI, dT, ds, s, d, "bf16")
+
+
+@pytest.mark.parametrize("s,sigma", [(1.0, 1.0), (14.29, 1.0), (50.0, 1.0), (100.0, 0.5)])
+def test_scales_bf16(s, sigma):
+    gpu, fwd, dI, dT, ds, s32 = _case(1536, 512, s, sigma=sigma, seed=7)
+    _check(gpu, fwd, dI, dT, ds, s32, 512, "bf16")
+
+
+def test_weak_positive_reading_bf16():
+    """Noise added to the unit vector itself: positives barely above the negatives."""
+    gpu, fwd, dI, dT, ds, s = _case(1200, 256, 14.29, mode="weak", seed=3)
+    _check(gpu, fwd, dI, dT, ds, s, 256, "bf16")
+
+
+def test_dloss_scaling_bf16():
+    gpu, fwd, dI, dT, ds, s = _case(700, 256, 20.0, dloss=-0.37, seed=5)
+    _check(gpu, fwd, dI, dT, ds, s, 256, "bf16")
+
+
+@pytest.mark.parametrize("b,d", [(1, 64), (17, 64), (300, 192), (1024, 512)])
+def test_fp32_inputs(b, d):
+    gpu, fwd, dI, dT, ds, s = _case(b, d, 1.0 / 0.07, dtype="f32", seed=b)
+    _check(gpu, fwd, dI, dT, ds, s, d, "f32")
+
+
+def test_config1_fp32_workload():
+    """b=1024, d=512, fp32, sigma=1, s=1/0.07, seed 0: the whole small workload."""
+    c = synth.CONFIGS[1]
+    gpu, fwd, dI, dT, ds, s = _case(c["b"], c["d"], c["scale"], sigma=c["sigma"], dtype="f32", seed=0)
+    _check(gpu, fwd, dI, dT, ds, s, c["d"], "f32")
+
+
+def test_deterministic_bitwise():
+    img, txt = synth.clip_pairs(3000, 256, 1.0, seed=11, dtype="bf16")
+    a = run(img, txt, "bf16", 14.29)
+    b = run(img, txt, "bf16", 14.29)
+    for k in ("loss64", "dscale"):
+        assert a[k] == b[k]
+    for k in ("lse_r", "lse_c", "ell_r", "ell_c", "dI", "dT"):
+        assert np.array_equal(a[k], b[k]), k
