@@ -58,39 +58,27 @@ __device__ __forceinline__ int bwd_g(int r) { return 4 * (r & 3) + ((r >> 2) & 3
 // 16s + 8h + t -- exactly the contraction slot t of GEMM2 step s.
 __device__ __forceinline__ int bwd_perm(int m) { return (m & 0x13) | ((m & 4) << 1) | ((m & 8) >> 1); }
 
-template <typename TIN, int D>
-__device__ __forceinline__ void bwd_tile_dma(const BwdParams& p, int64_t j0, INFCL_LDS char* buf, int wave,
-                                             int lane) {
-  constexpr int EPC = 16 / sizeof(TIN);
-  constexpr int CPR = D / EPC;               // chunks per row
-  constexpr int NI = kBwdBN * CPR / 64;      // DMA instructions per tile
-  static_assert(NI % 4 == 0, "tile DMA must split evenly over 4 waves");
-  const int64_t b = p.b;
-#pragma unroll
-  for (int kk = 0; kk < NI / 4; ++kk) {
-    const int k = wave + 4 * kk;
-    const int F = 64 * k + lane;
-    const int r = F / CPR, pc = F % CPR;
-    const int c = pc ^ bwd_g(r);
-    int64_t row = j0 + r;
-    row = row < b ? row : b - 1;
-    dma16((const TIN*)p.swept + row * D + c * EPC, (INFCL_LDS void*)(buf + 1024 * k));
-  }
-}
-
-template <typename TIN, int D, int FB>
+template <typename TIN, int D, int FB, bool PIPE>
 __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   constexpr int ES = sizeof(TIN);
+  constexpr int EPC = 16 / ES;          // elements per 16-byte chunk
   constexpr int KS = D / 16;            // 16-wide contraction steps of GEMM1
   constexpr int CPR = D * ES / 16;      // 16-byte chunks per swept row
   constexpr int ROWB = CPR * 16;        // bytes per swept row in LDS
   constexpr int TILEB = kBwdBN * ROWB;  // bytes per swept tile
+  constexpr int NI = TILEB / 1024;      // 1 KiB DMA instructions per tile
+  constexpr int NIW = NI / 4;           // ... per wave
   constexpr int FP = 32 * FB;           // features per pass
   constexpr int NPASS = D / FP;
+  // three tile buffers (t in GEMM2, t+1 in GEMM1, t+2 loading) when they fit,
+  // otherwise two (GEMM1 -> G' -> GEMM2 per tile while the next tile loads)
+  constexpr int NBUF = PIPE && 3 * (TILEB + 128) + 2048 <= 160 * 1024 ? 3 : 2;
   static_assert(D % FP == 0, "pass width must divide d");
-  static_assert(CPR % 16 == 0, "rows must hold a multiple of 16 chunks");
-  __shared__ __attribute__((aligned(1024))) char lds_[2 * TILEB];
+  static_assert(CPR % 16 == 0 && NI % 4 == 0, "rows must hold a multiple of 16 chunks");
+  static_assert(NBUF * (TILEB + 128) + 2048 <= 160 * 1024, "LDS budget");
+  __shared__ __attribute__((aligned(1024))) char lds_[NBUF * TILEB + NBUF * 128];
   INFCL_LDS char* lds = (INFCL_LDS char*)lds_;
+  INFCL_LDS char* lse_lds = lds + NBUF * TILEB;  // 32 swept log-sum-exp values per buffer
 
   const int lane = __lane_id();
   const int wave = threadIdx.x >> 6;
@@ -101,6 +89,7 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   const bool own_ok = iown < b;
   const int64_t irow = own_ok ? iown : b - 1;
   const bool wave_rows_ok = own0 + 32 <= b;
+  const int ntile = (int)((b + kBwdBN - 1) / kBwdBN);
 
   const float s = p.scale[0];
   const float k2 = s * kLog2e;
@@ -122,22 +111,41 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   const float uO = own_ok ? p.udiag[iown] : 0.f;
   const float gdiag = own_ok ? expm1f(-p.ell_own[iown]) + expm1f(-p.ell_swept[iown]) : 0.f;
 
+  // ---- DMA of a swept tile: instruction k = wave + 4 kk writes LDS bytes
+  // [1024 k, 1024 k + 1024) of the buffer; lane L fills physical chunk 64 k + L,
+  // i.e. row r = (64 k + L) / CPR, physical chunk pc = (64 k + L) % CPR, which
+  // holds logical chunk pc ^ g(r).  Per-lane byte offsets in the source rows:
+  uint32_t dma_off[NIW];
+#pragma unroll
+  for (int kk = 0; kk < NIW; ++kk) {
+    const int F = 64 * (wave + 4 * kk) + lane;
+    const int r = F / CPR, pc = F % CPR;
+    dma_off[kk] = (uint32_t)(r * D * ES + (pc ^ bwd_g(r)) * 16);
+  }
+  auto issue_tile = [&](int jt, int buf) {
+    const int64_t j0 = (int64_t)jt * kBwdBN;
+    INFCL_LDS char* dst = lds + buf * TILEB;
+    // rows past b fall outside the resource and load as zeros (their G' is masked)
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc((const char*)p.swept + j0 * (D * ES), (b - j0) * (D * ES));
+#pragma unroll
+    for (int kk = 0; kk < NIW; ++kk) dma16b(rs, (INFCL_LDS void*)(dst + 1024 * (wave + 4 * kk)), dma_off[kk], 0);
+    if (wave == 0 && lane < 8) {
+      const __amdgpu_buffer_rsrc_t rl = make_rsrc(p.lse_swept + j0, (b - j0) * 4);
+      dma16b(rl, (INFCL_LDS void*)(lse_lds + 128 * buf), 16u * lane, 0);
+    }
+  };
+
   // ---- per-lane LDS offsets; every read below is one of these plus an immediate
-  // GEMM1 (row-fragment) reads: swept row perm(l32), logical chunk 16*s_hi + cl,
-  // physical chunk 16*s_hi + (cl ^ g(row)).
-  constexpr int NA = ES == 2 ? 8 : 8;  // distinct cl patterns
-  int offA[NA];
+  int offA[8];
   {
     const int rA = bwd_perm(l32);
     const int gA = bwd_g(rA);
 #pragma unroll
-    for (int k = 0; k < NA; ++k) {
+    for (int k = 0; k < 8; ++k) {
       const int cl = ES == 2 ? (2 * k + h) : (4 * (k >> 1) + 2 * h + (k & 1));
       offA[k] = rA * ROWB + 16 * (cl ^ gA);
     }
   }
-  // GEMM2 transposing reads: row 16 s2 + 4 t + (8 hh + e), feature 32 fbabs + 16 nb16 + 4 qq
-  // -> physical chunk 16 (fbabs >> 2) + 4 ((fbabs & 3) ^ e) + (lo ^ ((t + 2 hh) & 3)).
   int offT[2][4];
   {
     const int g4 = lane >> 4, l16 = lane & 15;
@@ -150,18 +158,76 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
       for (int fm = 0; fm < 4; ++fm)
         offT[t][fm] = (8 * hh + e) * ROWB + 16 * (4 * (fm ^ e) + (lo ^ ((t + 2 * hh) & 3))) + fo;
   }
-  // fp32 GEMM2 reads: swept row jr(r, h), feature 32 fbabs + l32 -> chunk 8 fbabs + (l32 >> 2)
-  int offF[16];
-  if constexpr (ES == 4) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int j = bwd_perm(8 * (r >> 2) + 4 * h + (r & 3));
-      offF[r] = j * ROWB + (l32 & 3) * 4;  // chunk part added per feature block below
-    }
-  }
 
   double ds_acc = 0.0;
-  const int ntile = (int)((b + kBwdBN - 1) / kBwdBN);
+
+  // GEMM1 of swept tile jt (in buffer buf): S^T block, MFMA row m <-> swept row j0 + perm(m)
+  auto gemm1 = [&](int buf) {
+    const INFCL_LDS char* cur = lds + buf * TILEB;
+    f32x16 sacc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sacc[r] = 0.f;
+    if constexpr (ES == 2) {
+#pragma unroll
+      for (int s2 = 0; s2 < KS; ++s2) {
+        bf16x8 a = *(const INFCL_LDS bf16x8*)(cur + offA[s2 & 7] + 256 * (s2 >> 3));
+        sacc = mfma_bf16(a, ownf[s2][0], sacc);
+      }
+    } else {
+#pragma unroll
+      for (int s2 = 0; s2 < KS; ++s2) {
+        const int kb = 2 * (s2 & 3);
+        f32x4 a0 = *(const INFCL_LDS f32x4*)(cur + offA[kb] + 256 * (s2 >> 2));
+        f32x4 a1 = *(const INFCL_LDS f32x4*)(cur + offA[kb + 1] + 256 * (s2 >> 2));
+#pragma unroll
+        for (int t = 0; t < 4; ++t) sacc = mfma_f32(a0[t], ownf[s2][0][t], sacc);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) sacc = mfma_f32(a1[t], ownf[s2][1][t], sacc);
+      }
+    }
+    return sacc;
+  };
+
+  // G' of swept tile jt from its S^T block (log2 domain); entry r <-> swept row
+  // j = j0 + 16 (r>>3) + 8h + (r&7).  Returns the dscale contribution.
+  auto epilogue = [&](int jt, int buf, const f32x16& sacc, float (&gv)[16]) -> float {
+    const int64_t j0 = (int64_t)jt * kBwdBN;
+    float ds_tile = 0.f;
+    const bool special = (j0 == own0) || (j0 + kBwdBN > b) || !wave_rows_ok;
+    if (!special) {
+      float aS[16];
+      const INFCL_LDS char* lp = lse_lds + 128 * buf + 32 * h;
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const f32x4 v = *(const INFCL_LDS f32x4*)(lp + 64 * (q4 >> 1) + 16 * (q4 & 1));
+#pragma unroll
+        for (int c = 0; c < 4; ++c) aS[4 * q4 + c] = v[c] * kLog2e;
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float pO = exp2_hw(__builtin_fmaf(sacc[r], k2, -aO));
+        const float pS = exp2_hw(__builtin_fmaf(sacc[r], k2, -aS[r]));
+        gv[r] = pO + pS;
+        ds_tile = __builtin_fmaf(pO, sacc[r] - uO, ds_tile);
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t j = j0 + 16 * (r >> 3) + 8 * h + (r & 7);
+        const bool jok = j < b;
+        const float aSr = p.lse_swept[jok ? j : b - 1] * kLog2e;
+        const float pO = exp2_hw(__builtin_fmaf(sacc[r], k2, -aO));
+        const float pS = exp2_hw(__builtin_fmaf(sacc[r], k2, -aSr));
+        const bool ok = own_ok && jok;
+        const bool dg = (j == iown);
+        float gg = ok ? pO + pS : 0.f;
+        gg = dg ? gdiag : gg;
+        gv[r] = gg;
+        ds_tile += (ok && !dg) ? pO * (sacc[r] - uO) : 0.f;
+      }
+    }
+    return ds_tile;
+  };
 
   for (int pass = 0; pass < NPASS; ++pass) {
     f32x16 dacc[FB];
@@ -170,77 +236,9 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) dacc[fb][r] = 0.f;
 
-    bwd_tile_dma<TIN, D>(p, 0, lds, wave, lane);
-    wait_dma();
-    __syncthreads();
-
-    for (int jt = 0; jt < ntile; ++jt) {
-      const int cur_off = (jt & 1) * TILEB;
-      const INFCL_LDS char* cur = lds + cur_off;
-      if (jt + 1 < ntile) bwd_tile_dma<TIN, D>(p, (int64_t)(jt + 1) * kBwdBN, lds + (TILEB - cur_off), wave, lane);
-      const int64_t j0 = (int64_t)jt * kBwdBN;
-
-      // ---- GEMM1: S^T block, MFMA row m <-> swept row j0 + perm(m)
-      f32x16 sacc;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[r] = 0.f;
-      if constexpr (ES == 2) {
-#pragma unroll
-        for (int s2 = 0; s2 < KS; ++s2) {
-          bf16x8 a = *(const INFCL_LDS bf16x8*)(cur + offA[s2 & 7] + 256 * (s2 >> 3));
-          sacc = mfma_bf16(a, ownf[s2][0], sacc);
-        }
-      } else {
-#pragma unroll
-        for (int s2 = 0; s2 < KS; ++s2) {
-          const int kb = 2 * (s2 & 3);
-          f32x4 a0 = *(const INFCL_LDS f32x4*)(cur + offA[kb] + 256 * (s2 >> 2));
-          f32x4 a1 = *(const INFCL_LDS f32x4*)(cur + offA[kb + 1] + 256 * (s2 >> 2));
-#pragma unroll
-          for (int t = 0; t < 4; ++t) sacc = mfma_f32(a0[t], ownf[s2][0][t], sacc);
-#pragma unroll
-          for (int t = 0; t < 4; ++t) sacc = mfma_f32(a1[t], ownf[s2][1][t], sacc);
-        }
-      }
-
-      // ---- G' (log2 domain): entry r <-> swept row j = j0 + 16 (r>>3) + 8h + (r&7)
-      float gv[16];
-      float ds_tile = 0.f;
-      const bool special = (j0 == own0) || (j0 + kBwdBN > b) || !wave_rows_ok;
-      if (!special) {
-        float aS[16];
-#pragma unroll
-        for (int a4 = 0; a4 < 4; ++a4) {
-          f32x4 v = *(const f32x4*)(p.lse_swept + j0 + 16 * (a4 >> 1) + 8 * h + 4 * (a4 & 1));
-#pragma unroll
-          for (int c = 0; c < 4; ++c) aS[4 * a4 + c] = v[c] * kLog2e;
-        }
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float pO = exp2_hw(__builtin_fmaf(sacc[r], k2, -aO));
-          const float pS = exp2_hw(__builtin_fmaf(sacc[r], k2, -aS[r]));
-          gv[r] = pO + pS;
-          ds_tile = __builtin_fmaf(pO, sacc[r] - uO, ds_tile);
-        }
-      } else {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int64_t j = j0 + 16 * (r >> 3) + 8 * h + (r & 7);
-          const bool jok = j < b;
-          const float aSr = p.lse_swept[jok ? j : b - 1] * kLog2e;
-          const float pO = exp2_hw(__builtin_fmaf(sacc[r], k2, -aO));
-          const float pS = exp2_hw(__builtin_fmaf(sacc[r], k2, -aSr));
-          const bool ok = own_ok && jok;
-          const bool dg = (j == iown);
-          float gg = ok ? pO + pS : 0.f;
-          gg = dg ? gdiag : gg;
-          gv[r] = gg;
-          ds_tile += (ok && !dg) ? pO * (sacc[r] - uO) : 0.f;
-        }
-      }
-      if (pass == 0) ds_acc += (double)ds_tile;
-
-      // ---- GEMM2: dOwn(own rows x pass features) += G' * swept_tile
+    // GEMM2 of the tile in buffer buf with its G' (ga): dOwn += G' * swept_tile
+    auto gemm2 = [&](int buf, const float (&gv)[16]) {
+      const INFCL_LDS char* cur = lds + buf * TILEB;
       if constexpr (ES == 2) {
         bf16x8 ga[2];
 #pragma unroll
@@ -255,10 +253,9 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
 #pragma unroll
           for (int s2 = 0; s2 < 2; ++s2) {
             const int imm = 16 * s2 * ROWB + 256 * (fb >> 2);
-            s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (INFCL_LDS s16x4*)(curT + offT[0][fb & 3] + imm));
-            s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (INFCL_LDS s16x4*)(curT + offT[1][fb & 3] + 4 * ROWB + imm));
+            s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFCL_LDS s16x4*)(curT + offT[0][fb & 3] + imm));
+            s16x4 hi =
+                __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFCL_LDS s16x4*)(curT + offT[1][fb & 3] + 4 * ROWB + imm));
             typedef short s16x8 __attribute__((ext_vector_type(8)));
             s16x8 bb = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
             dacc[fb] = mfma_bf16(ga[s2], __builtin_bit_cast(bf16x8, bb), dacc[fb]);
@@ -273,14 +270,62 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
           for (int r = 0; r < 16; ++r) {
             const int j = bwd_perm(8 * (r >> 2) + 4 * h + (r & 3));
             const int cf = 8 * fbabs + (l32 >> 2);
-            float bv = *(const INFCL_LDS float*)(cur + offF[r] + 16 * (cf ^ bwd_g(j)));
+            float bv = *(const INFCL_LDS float*)(cur + j * ROWB + 16 * (cf ^ bwd_g(j)) + (l32 & 3) * 4);
             dacc[fb] = mfma_f32(gv[r], bv, dacc[fb]);
           }
         }
       }
+    };
 
+    if constexpr (NBUF == 2) {
+      issue_tile(0, 0);
       wait_dma();
       __syncthreads();
+      for (int jt = 0; jt < ntile; ++jt) {
+        const int bcur = jt & 1;
+        if (jt + 1 < ntile) issue_tile(jt + 1, bcur ^ 1);
+        float gv[16];
+        f32x16 sacc = gemm1(bcur);
+        const float d0 = epilogue(jt, bcur, sacc, gv);
+        if (pass == 0) ds_acc += (double)d0;
+        gemm2(bcur, gv);
+        wait_dma();
+        __syncthreads();
+      }
+    } else {
+    // prologue: tiles 0 and 1 in flight, tile 0's G' computed
+    issue_tile(0, 0);
+    if (ntile > 1) issue_tile(1, 1);
+    wait_dma();
+    __syncthreads();
+    float gcur[16];
+    {
+      f32x16 sacc = gemm1(0);
+      const float d0 = epilogue(0, 0, sacc, gcur);
+      if (pass == 0) ds_acc += (double)d0;
+    }
+
+    int bcur = 0;
+    for (int jt = 0; jt < ntile; ++jt) {
+      const int bnext = bcur == NBUF - 1 ? 0 : bcur + 1;
+      const int bload = bnext == NBUF - 1 ? 0 : bnext + 1;
+      if (jt + 2 < ntile) issue_tile(jt + 2, bload);
+      float gnext[16];
+      if (jt + 1 < ntile) {
+        // GEMM1 and G' of the next tile overlap GEMM2 of this one
+        f32x16 sacc = gemm1(bnext);
+        gemm2(bcur, gcur);
+        const float dn = epilogue(jt + 1, bnext, sacc, gnext);
+        if (pass == 0) ds_acc += (double)dn;
+      } else {
+        gemm2(bcur, gcur);
+      }
+      wait_dma();
+      __syncthreads();
+#pragma unroll
+      for (int r = 0; r < 16; ++r) gcur[r] = gnext[r];
+      bcur = bnext;
+    }
     }
 
     // ---- write dOwn rows of this pass: lane holds feature l32 of block fb, rows 8(r>>2)+4h+(r&3)
@@ -346,7 +391,7 @@ static int launch_bwd_d(const BwdParams& p, int nwg, hipStream_t stream) {
     return best;
   }();
   static_assert(ES == 4 || FB % 4 == 0, "bf16 pass width must be a multiple of 128 features");
-  hipLaunchKernelGGL((bwd_sweep<TIN, D, FB>), dim3(nwg), dim3(256), 0, stream, p);
+  hipLaunchKernelGGL((bwd_sweep<TIN, D, FB, false>), dim3(nwg), dim3(256), 0, stream, p);
   return hipGetLastError() == hipSuccess ? 0 : 1;
 }
 

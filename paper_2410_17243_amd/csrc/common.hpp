@@ -50,6 +50,18 @@ __device__ __forceinline__ void dma16(const void* gsrc, INFCL_LDS void* lds_base
 }
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// Raw buffer resource over [base, base + nbytes): loads past the end return 0.
+// Rebased per tile so that 32-bit per-lane offsets address inputs of any size.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t nbytes) {
+  const int64_t n = nbytes < 0 ? 0 : (nbytes > 0xFFFFFFF0ll ? 0xFFFFFFF0ll : nbytes);
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, (int)(uint32_t)n, 0x00020000);
+}
+// 16-byte buffer -> LDS copy; lane L writes LDS bytes [lds_base + 16 L, +16).
+__device__ __forceinline__ void dma16b(__amdgpu_buffer_rsrc_t rs, INFCL_LDS void* lds_base, uint32_t voff,
+                                       uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds_base, 16, voff, soff, 0, 0);
+}
+
 // Merge of two base-2 log-sum-exp pairs (R, l) -> (max R, rescaled sum).
 __device__ __forceinline__ void lse2_merge(float& R, float& l, float R2, float l2) {
   float M = fmaxf(R, R2);

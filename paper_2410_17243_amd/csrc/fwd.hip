@@ -54,30 +54,37 @@ constexpr int kFwdStageBytes = kFwdRows * 128;  // 128 bytes of every row per st
 // 16-byte chunk hit 16 distinct bank groups.
 __device__ __forceinline__ int fwd_swz(int r, int c) { return c ^ ((r >> 1) & 7); }
 
-// Issue the DMA of one K-stage (128 bytes of each of the 320 tile rows).
-template <typename TIN>
-__device__ __forceinline__ void fwd_stage_dma(const FwdParams& p, int64_t i0, int64_t j0, int st,
-                                              INFCL_LDS char* buf, int wave, int lane) {
-  constexpr int EPC = 16 / sizeof(TIN);  // elements per 16-byte chunk
-  constexpr int BK = 128 / sizeof(TIN);  // elements per stage
-  const int64_t b = p.b, d = p.d;
+// Per-lane source offsets of the K-stage DMA: instruction k (= wave + 4 kk)
+// fills tile rows 8k..8k+7; lane L copies logical chunk fwd_swz(r, L & 7) of row
+// r = 8k + L/8 to physical chunk L & 7.  Rows 0..63 are image rows, 64..319 text rows.
+struct FwdDmaOffsets {
+  uint32_t off[kFwdRows / 8 / 4];
+};
+
+__device__ __forceinline__ FwdDmaOffsets fwd_dma_offsets(int64_t d, int es, int wave, int lane) {
+  FwdDmaOffsets o;
 #pragma unroll
-  for (int kk = 0; kk < kFwdRows / 8 / 4; ++kk) {  // 10 instructions per wave
-    int k = wave + 4 * kk;
-    int r = 8 * k + (lane >> 3);
-    int c = fwd_swz(r, lane & 7);
-    const TIN* src;
-    if (r < kFwdBI) {
-      int64_t row = i0 + r;
-      row = row < b ? row : b - 1;
-      src = (const TIN*)p.img + row * d;
-    } else {
-      int64_t row = j0 + (r - kFwdBI);
-      row = row < b ? row : b - 1;
-      src = (const TIN*)p.txt + row * d;
-    }
-    dma16(src + (int64_t)st * BK + c * EPC, (INFCL_LDS void*)(buf + 1024 * k));
+  for (int kk = 0; kk < kFwdRows / 8 / 4; ++kk) {
+    const int k = wave + 4 * kk;
+    const int r = 8 * k + (lane >> 3);
+    const int rl = kk < 2 ? r : r - kFwdBI;  // row within the image or the text tile
+    o.off[kk] = (uint32_t)(rl * d * es + 16 * fwd_swz(r, lane & 7));
   }
+  return o;
+}
+
+// Issue the DMA of one K-stage (128 bytes of each of the 320 tile rows).  Rows
+// past b fall outside the buffer resources and load as zeros (they are masked).
+template <typename TIN>
+__device__ __forceinline__ void fwd_stage_dma(const FwdParams& p, const FwdDmaOffsets& o, int64_t i0, int64_t j0,
+                                              int st, INFCL_LDS char* buf, int wave) {
+  const int64_t b = p.b, rowb = p.d * (int64_t)sizeof(TIN);
+  const __amdgpu_buffer_rsrc_t ri = make_rsrc((const char*)p.img + i0 * rowb, (b - i0) * rowb);
+  const __amdgpu_buffer_rsrc_t rt = make_rsrc((const char*)p.txt + j0 * rowb, (b - j0) * rowb);
+  const uint32_t soff = (uint32_t)st * 128u;
+#pragma unroll
+  for (int kk = 0; kk < kFwdRows / 8 / 4; ++kk)
+    dma16b(kk < 2 ? ri : rt, (INFCL_LDS void*)(buf + 1024 * (wave + 4 * kk)), o.off[kk], soff);
 }
 
 // MFMA work of one K-stage: acc[mb][nb] += S^T block (j block mb, i block nb).
@@ -329,8 +336,9 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep(FwdParams p) {
     rowL[nb] = 0.f;
   }
 
+  const FwdDmaOffsets dmo = fwd_dma_offsets(p.d, (int)sizeof(TIN), wave, lane);
   int rr = 0, cc = 0;  // position of the current tile in this workgroup's (row, column) sweep
-  fwd_stage_dma<TIN>(p, (int64_t)q * kFwdBI, (int64_t)ct_lo * kFwdBJ, 0, lds0, wave, lane);
+  fwd_stage_dma<TIN>(p, dmo, (int64_t)q * kFwdBI, (int64_t)ct_lo * kFwdBJ, 0, lds0, wave);
   wait_dma();
   __syncthreads();
 
@@ -352,14 +360,14 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep(FwdParams p) {
         for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
 
     for (int st = 0; st < nst; st += 2) {
-      fwd_stage_dma<TIN>(p, i0, j0, st + 1, lds1, wave, lane);
+      fwd_stage_dma<TIN>(p, dmo, i0, j0, st + 1, lds1, wave);
       fwd_stage_mfma<TIN>(lds0, acc, wave, lane);
       wait_dma();
       __syncthreads();
       if (st + 2 < nst)
-        fwd_stage_dma<TIN>(p, i0, j0, st + 2, lds0, wave, lane);
+        fwd_stage_dma<TIN>(p, dmo, i0, j0, st + 2, lds0, wave);
       else if (has_next)
-        fwd_stage_dma<TIN>(p, ni0, nj0, 0, lds0, wave, lane);
+        fwd_stage_dma<TIN>(p, dmo, ni0, nj0, 0, lds0, wave);
       fwd_stage_mfma<TIN>(lds1, acc, wave, lane);
       if (st + 2 < nst) {
         wait_dma();
