@@ -42,13 +42,14 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build libinfcl.so)")
 
 
-def build(verbose: bool = False, resource_usage: bool = False) -> str:
+def build(verbose: bool = False, resource_usage: bool = False, defines=(), out: str = LIB) -> str:
+    """Compile and link; `defines` are extra -D options (build-time tuning knobs)."""
     cc = hipcc()
     tmp = tempfile.mkdtemp(prefix="infcl_build_")
     try:
         def compile_one(src):
             obj = os.path.join(tmp, src + ".o")
-            cmd = [cc, *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+            cmd = [cc, *HIPCC_FLAGS, *["-D" + x for x in defines], "-c", os.path.join(CSRC, src), "-o", obj]
             if resource_usage:
                 cmd.insert(1, "-Rpass-analysis=kernel-resource-usage")
             r = subprocess.run(cmd, capture_output=True, text=True)
@@ -61,20 +62,22 @@ def build(verbose: bool = False, resource_usage: bool = False) -> str:
         for _, err in results:
             if verbose and err.strip():
                 print(err, file=sys.stderr)
-        out_tmp = LIB + ".tmp"
+        out_tmp = out + ".tmp"
         cmd = [cc, "--offload-arch=gfx950", "-shared", "-fPIC", *[o for o, _ in results], "-o", out_tmp]
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:
             raise RuntimeError(f"link failed:\n{r.stderr}")
-        os.replace(out_tmp, LIB)
+        os.replace(out_tmp, out)
     finally:
         shutil.rmtree(tmp, ignore_errors=True)
-    return LIB
+    return out
 
 
 if __name__ == "__main__":
     ap = argparse.ArgumentParser()
     ap.add_argument("--verbose", action="store_true")
     ap.add_argument("--resource-usage", action="store_true")
+    ap.add_argument("-D", dest="defines", action="append", default=[], help="extra preprocessor define")
+    ap.add_argument("-o", dest="out", default=LIB)
     a = ap.parse_args()
-    print(build(verbose=a.verbose or a.resource_usage, resource_usage=a.resource_usage))
+    print(build(verbose=a.verbose or a.resource_usage, resource_usage=a.resource_usage, defines=a.defines, out=a.out))

@@ -47,6 +47,18 @@ struct BwdParams {
 };
 
 constexpr int kBwdBM = 128;  // own rows per workgroup (32 per wave)
+
+// LDS read-ahead (steps) of the two products and the number of independent
+// accumulation chains of the first one (build-time tuning knobs).
+#ifndef INFCL_BWD_G1_PRE
+#define INFCL_BWD_G1_PRE 4
+#endif
+#ifndef INFCL_BWD_G1_CHAINS
+#define INFCL_BWD_G1_CHAINS 1
+#endif
+#ifndef INFCL_BWD_G2_PRE
+#define INFCL_BWD_G2_PRE 3
+#endif
 constexpr int kBwdBN = 32;   // swept rows per tile
 
 // Chunk swizzle for the swept tile (rows of >= 16 chunks): 16 rows reading one
@@ -58,7 +70,7 @@ __device__ __forceinline__ int bwd_g(int r) { return 4 * (r & 3) + ((r >> 2) & 3
 // 16s + 8h + t -- exactly the contraction slot t of GEMM2 step s.
 __device__ __forceinline__ int bwd_perm(int m) { return (m & 0x13) | ((m & 4) << 1) | ((m & 8) >> 1); }
 
-template <typename TIN, int D, int FB, bool PIPE>
+template <typename TIN, int D, int FB, bool PIPE, int RING>
 __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   constexpr int ES = sizeof(TIN);
   constexpr int EPC = 16 / ES;          // elements per 16-byte chunk
@@ -72,11 +84,17 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   constexpr int NPASS = D / FP;
   // three tile buffers (t in GEMM2, t+1 in GEMM1, t+2 loading) when they fit,
   // otherwise two (GEMM1 -> G' -> GEMM2 per tile while the next tile loads)
-  constexpr int NBUF = PIPE && 3 * (TILEB + 128) + 2048 <= 160 * 1024 ? 3 : 2;
+  // PIPE: three tile buffers (t in GEMM2, t+1 in GEMM1, t+2 loading).
+  // Otherwise a ring of RING buffers: GEMM1 -> G' -> GEMM2 per tile while the
+  // next RING-1 tiles load (clamped to what fits in LDS).
+  constexpr int GPB = ES == 2 ? kBwdBM * kBwdBN * 2 : 0;  // G' exchange buffer bytes
+  constexpr int RINGFIT = (160 * 1024 - 2048 - GPB) / (TILEB + 128);
+  constexpr int NBUF = PIPE ? 3 : (RING < RINGFIT ? RING : RINGFIT);
+  static_assert(NBUF >= 2, "at least two tile buffers");
   static_assert(D % FP == 0, "pass width must divide d");
   static_assert(CPR % 16 == 0 && NI % 4 == 0, "rows must hold a multiple of 16 chunks");
-  static_assert(NBUF * (TILEB + 128) + 2048 <= 160 * 1024, "LDS budget");
-  __shared__ __attribute__((aligned(1024))) char lds_[NBUF * TILEB + NBUF * 128];
+  static_assert(NBUF * (TILEB + 128) + GPB + 2048 <= 160 * 1024, "LDS budget");
+  __shared__ __attribute__((aligned(1024))) char lds_[NBUF * TILEB + NBUF * 128 + GPB];
   INFCL_LDS char* lds = (INFCL_LDS char*)lds_;
   INFCL_LDS char* lse_lds = lds + NBUF * TILEB;  // 32 swept log-sum-exp values per buffer
 
@@ -114,66 +132,104 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   // ---- DMA of a swept tile: instruction k = wave + 4 kk writes LDS bytes
   // [1024 k, 1024 k + 1024) of the buffer; lane L fills physical chunk 64 k + L,
   // i.e. row r = (64 k + L) / CPR, physical chunk pc = (64 k + L) % CPR, which
-  // holds logical chunk pc ^ g(r).  Per-lane byte offsets in the source rows:
-  uint32_t dma_off[NIW];
-#pragma unroll
-  for (int kk = 0; kk < NIW; ++kk) {
-    const int F = 64 * (wave + 4 * kk) + lane;
-    const int r = F / CPR, pc = F % CPR;
-    dma_off[kk] = (uint32_t)(r * D * ES + (pc ^ bwd_g(r)) * 16);
-  }
+  // holds logical chunk pc ^ g(r).  The per-lane source offsets are recomputed
+  // at every issue from an opaque copy of the lane id: hoisted out of the loop
+  // they would be spilled, and a scratch reload waits for all in-flight DMA.
   auto issue_tile = [&](int jt, int buf) {
     const int64_t j0 = (int64_t)jt * kBwdBN;
     INFCL_LDS char* dst = lds + buf * TILEB;
+    int lo = lane;
+    asm volatile("" : "+v"(lo));
     // rows past b fall outside the resource and load as zeros (their G' is masked)
     const __amdgpu_buffer_rsrc_t rs = make_rsrc((const char*)p.swept + j0 * (D * ES), (b - j0) * (D * ES));
 #pragma unroll
-    for (int kk = 0; kk < NIW; ++kk) dma16b(rs, (INFCL_LDS void*)(dst + 1024 * (wave + 4 * kk)), dma_off[kk], 0);
+    for (int kk = 0; kk < NIW; ++kk) {
+      const int F = 64 * (wave + 4 * kk) + lo;
+      const int r = F / CPR, pc = F % CPR;
+      const uint32_t off = (uint32_t)(r * D * ES + (pc ^ bwd_g(r)) * 16);
+      dma16b(rs, (INFCL_LDS void*)(dst + 1024 * (wave + 4 * kk)), off, 0);
+    }
     if (wave == 0 && lane < 8) {
       const __amdgpu_buffer_rsrc_t rl = make_rsrc(p.lse_swept + j0, (b - j0) * 4);
-      dma16b(rl, (INFCL_LDS void*)(lse_lds + 128 * buf), 16u * lane, 0);
+      dma16b(rl, (INFCL_LDS void*)(lse_lds + 128 * buf), 16u * lo, 0);
     }
   };
 
-  // ---- per-lane LDS offsets; every read below is one of these plus an immediate
-  int offA[8];
-  {
-    const int rA = bwd_perm(l32);
+  // ---- per-lane LDS offsets; every read below is one of these plus an
+  // immediate.  They are rebuilt from an opaque lane id inside every tile
+  // iteration (see issue_tile for why nothing lane-dependent may stay live).
+  auto make_offA = [&](int lo, int (&offA)[8]) {
+    const int l32o = lo & 31, ho = lo >> 5;
+    const int rA = bwd_perm(l32o);
     const int gA = bwd_g(rA);
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-      const int cl = ES == 2 ? (2 * k + h) : (4 * (k >> 1) + 2 * h + (k & 1));
+      const int cl = ES == 2 ? (2 * k + ho) : (4 * (k >> 1) + 2 * ho + (k & 1));
       offA[k] = rA * ROWB + 16 * (cl ^ gA);
     }
-  }
-  int offT[2][4];
-  {
-    const int g4 = lane >> 4, l16 = lane & 15;
+  };
+  auto make_offT = [&](int lo, int (&offT)[2][4]) {
+    const int g4 = lo >> 4, l16 = lo & 15;
     const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
-    const int lo = 2 * nb16 + (qq >> 1);
+    const int lb = 2 * nb16 + (qq >> 1);
     const int fo = (qq & 1) * 8;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int fm = 0; fm < 4; ++fm)
-        offT[t][fm] = (8 * hh + e) * ROWB + 16 * (4 * (fm ^ e) + (lo ^ ((t + 2 * hh) & 3))) + fo;
-  }
+        offT[t][fm] = (8 * hh + e) * ROWB + 16 * (4 * (fm ^ e) + (lb ^ ((t + 2 * hh) & 3))) + fo;
+  };
+  auto opaque_lane = [&]() {
+    int lo = lane;
+    asm volatile("" : "+v"(lo));
+    return lo;
+  };
 
   double ds_acc = 0.0;
 
-  // GEMM1 of swept tile jt (in buffer buf): S^T block, MFMA row m <-> swept row j0 + perm(m)
+  // GEMM1 of swept tile jt (in buffer buf): S^T block, MFMA row m <-> swept row j0 + perm(m).
+  // bf16: LDS fragments are read kPre steps ahead of their MFMA through a
+  // register ring, and the steps alternate between two accumulators so that
+  // consecutive MFMAs are independent; the scheduling groups pin the order
+  // MFMA, read, MFMA, read, ...
   auto gemm1 = [&](int buf) {
     const INFCL_LDS char* cur = lds + buf * TILEB;
+    int offA[8];
+    make_offA(opaque_lane(), offA);
     f32x16 sacc;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) sacc[r] = 0.f;
     if constexpr (ES == 2) {
+      constexpr int kPre = KS < INFCL_BWD_G1_PRE ? KS : INFCL_BWD_G1_PRE;
+      constexpr int NCH = INFCL_BWD_G1_CHAINS;
+      f32x16 acc2[NCH];
+#pragma unroll
+      for (int c = 0; c < NCH; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc2[c][r] = 0.f;
+      bf16x8 ring[kPre];
+#pragma unroll
+      for (int i = 0; i < kPre; ++i) ring[i] = *(const INFCL_LDS bf16x8*)(cur + offA[i & 7] + 256 * (i >> 3));
+      __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
 #pragma unroll
       for (int s2 = 0; s2 < KS; ++s2) {
-        bf16x8 a = *(const INFCL_LDS bf16x8*)(cur + offA[s2 & 7] + 256 * (s2 >> 3));
-        sacc = mfma_bf16(a, ownf[s2][0], sacc);
+        const bf16x8 a = ring[s2 % kPre];
+        acc2[s2 % NCH] = mfma_bf16(a, ownf[s2][0], acc2[s2 % NCH]);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (s2 + kPre < KS) {
+          const int n = s2 + kPre;
+          ring[s2 % kPre] = *(const INFCL_LDS bf16x8*)(cur + offA[n & 7] + 256 * (n >> 3));
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float v = acc2[0][r];
+#pragma unroll
+        for (int c = 1; c < NCH; ++c) v += acc2[c][r];
+        sacc[r] = v;
       }
     } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[r] = 0.f;
 #pragma unroll
       for (int s2 = 0; s2 < KS; ++s2) {
         const int kb = 2 * (s2 & 3);
@@ -196,7 +252,7 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
     const bool special = (j0 == own0) || (j0 + kBwdBN > b) || !wave_rows_ok;
     if (!special) {
       float aS[16];
-      const INFCL_LDS char* lp = lse_lds + 128 * buf + 32 * h;
+      const INFCL_LDS char* lp = lse_lds + 128 * buf + 32 * (opaque_lane() >> 5);
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4) {
         const f32x4 v = *(const INFCL_LDS f32x4*)(lp + 64 * (q4 >> 1) + 16 * (q4 & 1));
@@ -229,119 +285,143 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
     return ds_tile;
   };
 
-  for (int pass = 0; pass < NPASS; ++pass) {
-    f32x16 dacc[FB];
-#pragma unroll
-    for (int fb = 0; fb < FB; ++fb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) dacc[fb][r] = 0.f;
+  // G' exchange buffer (bf16): [128 own rows][32 swept rows], 64-byte rows whose
+  // four 16-byte chunks are XOR-swizzled by (row >> 2) & 3.
+  constexpr int FBW = ES == 2 ? FB / 4 : FB;  // 32-feature blocks per wave and pass (bf16)
+  INFCL_LDS char* gp_lds = lse_lds + NBUF * 128;
+  auto gp_off = [](int row, int c) { return row * 64 + 16 * (c ^ ((row >> 2) & 3)); };
 
-    // GEMM2 of the tile in buffer buf with its G' (ga): dOwn += G' * swept_tile
-    auto gemm2 = [&](int buf, const float (&gv)[16]) {
+  for (int pass = 0; pass < NPASS; ++pass) {
+    // bf16: dacc[ob * FBW + fbw] holds own block ob (rows 32 ob .. of the
+    // workgroup) x feature block (pass FB + wave FBW + fbw).
+    // fp32: dacc[fb] holds this wave's own rows x feature block (pass FB + fb).
+    f32x16 dacc[ES == 2 ? 4 * FBW : FB];
+#pragma unroll
+    for (int i = 0; i < (ES == 2 ? 4 * FBW : FB); ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dacc[i][r] = 0.f;
+
+    // bf16 GEMM2: every wave multiplies the G' of all four waves (from LDS) by
+    // its quarter of the pass's features of the swept tile (transposing reads).
+    auto gemm2_bf16 = [&](int buf) {
       const INFCL_LDS char* cur = lds + buf * TILEB;
-      if constexpr (ES == 2) {
-        bf16x8 ga[2];
+      const int lo = opaque_lane();
+      const int l32o = lo & 31, ho = lo >> 5;
+      const int g4 = lo >> 4, l16 = lo & 15;
+      const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
+      const int lb = 2 * nb16 + (qq >> 1);
+      const int fo = (qq & 1) * 8;
+      // B-fragment offsets of this wave's feature blocks (read t = 0, 1)
+      int offB[2][FBW];
 #pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2)
+      for (int fbw = 0; fbw < FBW; ++fbw) {
+        const int fbabs = pass * FB + wave * FBW + fbw;
 #pragma unroll
-          for (int t = 0; t < 8; ++t) ga[s2][t] = (__bf16)gv[8 * s2 + t];
-        // FB is a multiple of 4, so feature block pass*FB+fb has low bits fb&3 and
-        // its chunk group (>> 2) splits into a per-pass base and an immediate.
-        const INFCL_LDS char* curT = cur + 64 * FB * pass;
+        for (int t = 0; t < 2; ++t)
+          offB[t][fbw] = (8 * hh + 4 * t + e) * ROWB +
+                         16 * (16 * (fbabs >> 2) + 4 * ((fbabs & 3) ^ e) + (lb ^ ((t + 2 * hh) & 3))) + fo;
+      }
+      typedef short s16x8 __attribute__((ext_vector_type(8)));
 #pragma unroll
-        for (int fb = 0; fb < FB; ++fb) {
+      for (int s2 = 0; s2 < 2; ++s2) {
+        bf16x8 A[4];
 #pragma unroll
-          for (int s2 = 0; s2 < 2; ++s2) {
-            const int imm = 16 * s2 * ROWB + 256 * (fb >> 2);
-            s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFCL_LDS s16x4*)(curT + offT[0][fb & 3] + imm));
-            s16x4 hi =
-                __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFCL_LDS s16x4*)(curT + offT[1][fb & 3] + 4 * ROWB + imm));
-            typedef short s16x8 __attribute__((ext_vector_type(8)));
-            s16x8 bb = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-            dacc[fb] = mfma_bf16(ga[s2], __builtin_bit_cast(bf16x8, bb), dacc[fb]);
-          }
-        }
-      } else {
-        // fp32: step r contracts swept row jr(r, h) of each lane half
+        for (int ob = 0; ob < 4; ++ob) A[ob] = *(const INFCL_LDS bf16x8*)(gp_lds + gp_off(32 * ob + l32o, 2 * s2 + ho));
 #pragma unroll
-        for (int fb = 0; fb < FB; ++fb) {
-          const int fbabs = pass * FB + fb;
+        for (int fbw = 0; fbw < FBW; ++fbw) {
+          const int imm = 16 * s2 * ROWB;
+          s16x4 b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFCL_LDS s16x4*)(cur + offB[0][fbw] + imm));
+          s16x4 b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFCL_LDS s16x4*)(cur + offB[1][fbw] + imm));
+          const s16x8 bb = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int j = bwd_perm(8 * (r >> 2) + 4 * h + (r & 3));
-            const int cf = 8 * fbabs + (l32 >> 2);
-            float bv = *(const INFCL_LDS float*)(cur + j * ROWB + 16 * (cf ^ bwd_g(j)) + (l32 & 3) * 4);
-            dacc[fb] = mfma_f32(gv[r], bv, dacc[fb]);
-          }
+          for (int ob = 0; ob < 4; ++ob)
+            dacc[ob * FBW + fbw] = mfma_bf16(A[ob], __builtin_bit_cast(bf16x8, bb), dacc[ob * FBW + fbw]);
         }
       }
     };
 
-    if constexpr (NBUF == 2) {
-      issue_tile(0, 0);
-      wait_dma();
-      __syncthreads();
-      for (int jt = 0; jt < ntile; ++jt) {
-        const int bcur = jt & 1;
-        if (jt + 1 < ntile) issue_tile(jt + 1, bcur ^ 1);
-        float gv[16];
-        f32x16 sacc = gemm1(bcur);
-        const float d0 = epilogue(jt, bcur, sacc, gv);
-        if (pass == 0) ds_acc += (double)d0;
-        gemm2(bcur, gv);
-        wait_dma();
-        __syncthreads();
+    // fp32 GEMM2: this wave's own rows x all the pass's features; step r
+    // contracts swept row jr(r, h) of each lane half.
+    auto gemm2_f32 = [&](int buf, const float (&gv)[16]) {
+      const INFCL_LDS char* cur = lds + buf * TILEB;
+#pragma unroll
+      for (int fb = 0; fb < FB; ++fb) {
+        const int fbabs = pass * FB + fb;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int j = bwd_perm(8 * (r >> 2) + 4 * h + (r & 3));
+          const int cf = 8 * fbabs + (l32 >> 2);
+          float bv = *(const INFCL_LDS float*)(cur + j * ROWB + 16 * (cf ^ bwd_g(j)) + (l32 & 3) * 4);
+          dacc[fb] = mfma_f32(gv[r], bv, dacc[fb]);
+        }
       }
-    } else {
-    // prologue: tiles 0 and 1 in flight, tile 0's G' computed
-    issue_tile(0, 0);
-    if (ntile > 1) issue_tile(1, 1);
+    };
+
+    // DMA instructions this wave issues per tile (wave 0 also copies the tile's
+    // log-sum-exp values): the wait before a tile's last barrier lets the
+    // NBUF-2 younger tiles stay in flight.
+    for (int k = 0; k < NBUF - 1; ++k)
+      if (k < ntile) issue_tile(k, k);
     wait_dma();
     __syncthreads();
-    float gcur[16];
-    {
-      f32x16 sacc = gemm1(0);
-      const float d0 = epilogue(0, 0, sacc, gcur);
-      if (pass == 0) ds_acc += (double)d0;
-    }
-
     int bcur = 0;
     for (int jt = 0; jt < ntile; ++jt) {
-      const int bnext = bcur == NBUF - 1 ? 0 : bcur + 1;
-      const int bload = bnext == NBUF - 1 ? 0 : bnext + 1;
-      if (jt + 2 < ntile) issue_tile(jt + 2, bload);
-      float gnext[16];
-      if (jt + 1 < ntile) {
-        // GEMM1 and G' of the next tile overlap GEMM2 of this one
-        f32x16 sacc = gemm1(bnext);
-        gemm2(bcur, gcur);
-        const float dn = epilogue(jt + 1, bnext, sacc, gnext);
-        if (pass == 0) ds_acc += (double)dn;
-      } else {
-        gemm2(bcur, gcur);
-      }
-      wait_dma();
-      __syncthreads();
+      const int bload = bcur == 0 ? NBUF - 1 : bcur - 1;  // buffer of tile jt-1, free since the last barrier
+      if (jt + NBUF - 1 < ntile) issue_tile(jt + NBUF - 1, bload);
+      float gv[16];
+      f32x16 sacc = gemm1(bcur);
+      const float d0 = epilogue(jt, bcur, sacc, gv);
+      if (pass == 0) ds_acc += (double)d0;
+      if constexpr (ES == 2) {
+        // publish this wave's G' rows (bf16): chunk 2 s2 + h of row 32 wave + l32
+        const int lo = opaque_lane();
+        const int rowg = 32 * wave + (lo & 31);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) gcur[r] = gnext[r];
-      bcur = bnext;
-    }
+        for (int s2 = 0; s2 < 2; ++s2) {
+          bf16x8 ga;
+#pragma unroll
+          for (int t = 0; t < 8; ++t) ga[t] = (__bf16)gv[8 * s2 + t];
+          *(INFCL_LDS bf16x8*)(gp_lds + gp_off(rowg, 2 * s2 + (lo >> 5))) = ga;
+        }
+        __syncthreads();
+        gemm2_bf16(bcur);
+      } else {
+        gemm2_f32(bcur, gv);
+      }
+      // tile jt+1 must be in LDS; tiles jt+2 .. jt+NBUF-1 may still load
+      const int younger = (ntile - 1 - (jt + 1)) < (NBUF - 2) ? (ntile - 1 - (jt + 1)) : (NBUF - 2);
+      if (younger <= 0) {
+        wait_dma();
+      } else {
+        wait_dma_allow(younger * (NIW + (wave == 0 ? 1 : 0)));
+      }
+      __syncthreads();
+      bcur = bcur == NBUF - 1 ? 0 : bcur + 1;
     }
 
-    // ---- write dOwn rows of this pass: lane holds feature l32 of block fb, rows 8(r>>2)+4h+(r&3)
-    float* dst = p.dOwn + (own0 + 4 * h) * D + 32 * pass * FB + l32;
-    if (wave_rows_ok) {
+    // ---- write dOwn: lane holds feature l32 of a 32-feature block, rows 8(r>>2)+4h+(r&3)
+    if constexpr (ES == 2) {
+      const int64_t wg0 = (int64_t)blockIdx.x * kBwdBM;
+      const bool all_ok = wg0 + kBwdBM <= b;
 #pragma unroll
-      for (int fb = 0; fb < FB; ++fb)
+      for (int ob = 0; ob < 4; ++ob) {
+        float* dst = p.dOwn + (wg0 + 32 * ob + 4 * h) * D + 32 * (pass * FB + wave * FBW) + l32;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fb] = kfin * dacc[fb][r];
+        for (int fbw = 0; fbw < FBW; ++fbw)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int64_t row = wg0 + 32 * ob + 8 * (r >> 2) + 4 * h + (r & 3);
+            if (all_ok || row < b) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fbw] = kfin * dacc[ob * FBW + fbw][r];
+          }
+      }
     } else {
+      float* dst = p.dOwn + (own0 + 4 * h) * D + 32 * pass * FB + l32;
 #pragma unroll
       for (int fb = 0; fb < FB; ++fb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int64_t row = own0 + 8 * (r >> 2) + 4 * h + (r & 3);
-          if (row < b) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fb] = kfin * dacc[fb][r];
+          if (wave_rows_ok || row < b) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fb] = kfin * dacc[fb][r];
         }
     }
   }
@@ -378,20 +458,32 @@ __global__ void __launch_bounds__(256) dscale_finish(const double* part, int64_t
 // Pass width: largest FB (32-feature blocks) dividing d/32 whose accumulators
 // (16 FB registers) fit next to the own operand (d/4 or d/2 registers); for
 // bf16 FB is also a multiple of 4 (see the transposing-read addressing).
+// Build-time tuning knobs: the register budget shared by the own operand and
+// the gradient accumulators, and whether the three-buffer pipeline is used.
+#ifndef INFCL_BWD_REG_BUDGET
+#define INFCL_BWD_REG_BUDGET 384
+#endif
+#ifndef INFCL_BWD_PIPE
+#define INFCL_BWD_PIPE 0
+#endif
+#ifndef INFCL_BWD_RING
+#define INFCL_BWD_RING 2
+#endif
+
 template <typename TIN, int D>
 static int launch_bwd_d(const BwdParams& p, int nwg, hipStream_t stream) {
   constexpr int ES = sizeof(TIN);
   constexpr int OWNREGS = D * ES / 8;
   constexpr int NB32 = D / 32;
-  constexpr int FBMAX = (384 - OWNREGS) / 16;
+  constexpr int FBMAX = (INFCL_BWD_REG_BUDGET - OWNREGS) / 16;
   constexpr int FB = [] {
-    int best = 1;
+    int best = ES == 4 ? 1 : 4;  // bf16: at least one 128-feature group
     for (int f = 1; f <= NB32; ++f)
       if (NB32 % f == 0 && f <= FBMAX && (ES == 4 || f % 4 == 0)) best = f;
     return best;
   }();
   static_assert(ES == 4 || FB % 4 == 0, "bf16 pass width must be a multiple of 128 features");
-  hipLaunchKernelGGL((bwd_sweep<TIN, D, FB, false>), dim3(nwg), dim3(256), 0, stream, p);
+  hipLaunchKernelGGL((bwd_sweep<TIN, D, FB, INFCL_BWD_PIPE != 0, INFCL_BWD_RING>), dim3(nwg), dim3(256), 0, stream, p);
   return hipGetLastError() == hipSuccess ? 0 : 1;
 }
 

@@ -49,6 +49,25 @@ __device__ __forceinline__ void dma16(const void* gsrc, INFCL_LDS void* lds_base
   __builtin_amdgcn_global_load_lds((const INFCL_GLOBAL void*)gsrc, lds_base, 16, 0, 0);
 }
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Wait until at most n (0..63) vector-memory operations of this wave are in
+// flight.  Operations complete in issue order, so this waits for all but the n
+// most recently issued ones.
+__device__ __forceinline__ void wait_dma_allow(int n) {
+  switch (n) {
+#define INFCL_VM_CASE(k) \
+  case k: asm volatile("s_waitcnt vmcnt(" #k ")" ::: "memory"); break;
+    INFCL_VM_CASE(0) INFCL_VM_CASE(1) INFCL_VM_CASE(2) INFCL_VM_CASE(3) INFCL_VM_CASE(4) INFCL_VM_CASE(5)
+    INFCL_VM_CASE(6) INFCL_VM_CASE(7) INFCL_VM_CASE(8) INFCL_VM_CASE(9) INFCL_VM_CASE(10) INFCL_VM_CASE(11)
+    INFCL_VM_CASE(12) INFCL_VM_CASE(13) INFCL_VM_CASE(14) INFCL_VM_CASE(15) INFCL_VM_CASE(16) INFCL_VM_CASE(17)
+    INFCL_VM_CASE(18) INFCL_VM_CASE(19) INFCL_VM_CASE(20) INFCL_VM_CASE(21) INFCL_VM_CASE(22) INFCL_VM_CASE(23)
+    INFCL_VM_CASE(24) INFCL_VM_CASE(25) INFCL_VM_CASE(26) INFCL_VM_CASE(27) INFCL_VM_CASE(28) INFCL_VM_CASE(29)
+    INFCL_VM_CASE(30) INFCL_VM_CASE(31) INFCL_VM_CASE(32) INFCL_VM_CASE(33) INFCL_VM_CASE(34) INFCL_VM_CASE(35)
+    INFCL_VM_CASE(36) INFCL_VM_CASE(37) INFCL_VM_CASE(38) INFCL_VM_CASE(39) INFCL_VM_CASE(40) INFCL_VM_CASE(41)
+    INFCL_VM_CASE(42) INFCL_VM_CASE(43) INFCL_VM_CASE(44) INFCL_VM_CASE(45) INFCL_VM_CASE(46) INFCL_VM_CASE(47)
+#undef INFCL_VM_CASE
+    default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+  }
+}
 
 // Raw buffer resource over [base, base + nbytes): loads past the end return 0.
 // Rebased per tile so that 32-bit per-lane offsets address inputs of any size.
