@@ -12,7 +12,7 @@ int launch_fwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype
                float* rowR, float* rowL, float* colR, float* colL, float* udiag, double* partial);
 int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale,
                const float* lse_r, const float* lse_c, const float* aux, const float* dloss, float* dimg, float* dtxt,
-               float* dscale, double* ds_part, hipStream_t stream);
+               float* dscale, float* lse2, double* ds_part, hipStream_t stream);
 bool bwd_supported(int64_t d, int dtype);
 }  // namespace infcl
 
@@ -22,7 +22,7 @@ constexpr int64_t kMaxB = (int64_t)1 << 30;
 
 struct Layout {
   int Pr, Pc;
-  size_t rowR, rowL, colR, colL, udiag, fwd_part, bwd_part, total;
+  size_t rowR, rowL, colR, colL, udiag, fwd_part, lse2, bwd_part, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -42,6 +42,7 @@ Layout make_layout(int64_t b) {
   L.colL = off; off = align256(off + (size_t)L.Pr * fb);
   L.udiag = off; off = align256(off + fb);
   L.fwd_part = off; off = align256(off + (size_t)((b + 255) / 256) * sizeof(double));
+  L.lse2 = off; off = align256(off + 2 * fb);
   L.bwd_part = off; off = align256(off + (size_t)2 * ((b + 127) / 128) * sizeof(double));
   L.total = off;
   return L;
@@ -96,7 +97,7 @@ infcl_status infcl_bwd(const void* img, const void* txt, int64_t b, int64_t d, i
   if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)workspace;
   int rc = infcl::launch_bwd(img, txt, b, d, dtype, scale, lse_r, lse_c, aux, dloss, dimg, dtxt, dscale,
-                             (double*)(ws + L.bwd_part), (hipStream_t)stream);
+                             (float*)(ws + L.lse2), (double*)(ws + L.bwd_part), (hipStream_t)stream);
   if (rc == 2) return INFCL_ERR_UNSUPPORTED;
   return rc == 0 ? INFCL_OK : INFCL_ERR_HIP;
 }

@@ -5,7 +5,7 @@
 // algorithm recomputes every tile from the saved log-sum-exp vectors):
 //   dL/dx_ij = (1/2b) (P^r_ij + P^c_ij) - (1/b) delta_ij,
 //   P^r_ij = exp(x_ij - r_i),  P^c_ij = exp(x_ij - c_j),
-//   dimg = dloss * s * G img-side = k * G' txt,   dtxt = k * G'^T img,
+//   dimg = k * G' txt,   dtxt = k * G'^T img,
 //   with G' = P^r + P^c off the diagonal, G'_ii = expm1(-(r_i-x_ii)) + expm1(-(c_i-x_ii)),
 //   k = dloss * s / (2b), and
 //   ds = dloss/(2b) * sum_{i != j} [P^r_ij (u_ij - u_ii) + P^c_ij (u_ij - u_jj)],  u = <img_i, txt_j>.
@@ -13,18 +13,28 @@
 // Design (differs from the paper's single pass that read-modify-writes the text
 // gradient tile in HBM for every tile): one kernel template, launched twice.
 // The launch that "owns" the image rows keeps dimg rows in registers and sweeps
-// all text rows; the second launch swaps the roles (owns text rows, sweeps
-// image rows).  The similarity tile is recomputed in each launch, but no
-// gradient ever leaves the registers before the sweep ends and no atomics are
-// used.  Per tile and wave:
+// all text rows; the second launch swaps the roles.  The similarity tile is
+// recomputed in each launch, but no gradient leaves the registers before the
+// sweep ends and no atomics are used.  A workgroup owns 128 rows (32 per wave)
+// and sweeps 32-row tiles of the other side.  Per tile and wave:
 //   GEMM1  S^T(32 swept x 32 own) = swept_tile * own^T   (own operand held in
 //          registers for the whole sweep, swept rows read from LDS with a
 //          row permutation that makes the accumulator usable as GEMM2's operand)
 //   G'     two exp2 per entry (log2 domain), the diagonal from expm1 terms
-//   GEMM2  dOwn(32 own x FP features) += G'(bf16) * swept_tile, the swept tile
-//          read feature-major through the transposing LDS read.
+//   GEMM2  bf16: the four waves' G' blocks are exchanged through LDS and each
+//          wave multiplies all 128 own rows by its quarter of the features;
+//          fp32: each wave multiplies its own 32 rows by all features.
 // Feature widths whose accumulators do not fit the register file are split in
-// passes of FP features; each pass recomputes GEMM1.
+// passes; each pass recomputes GEMM1.
+//
+// Memory pipeline.  Tiles arrive by LDS DMA (buffer loads that write LDS).
+// Each tile buffer, its log-sum-exp slot and the G' buffers are separate LDS
+// objects and the tile loop is unrolled over the buffer rotation, so every
+// LDS address is tied to one object at compile time: the compiler can then
+// see that the reads of the current tiles never alias the DMA in flight and
+// does not stall them on it.  The DMA instructions of the next tile are
+// spread over the MFMAs of GEMM1 (a burst fills the address queue and stalls
+// every wave at issue).
 #include <type_traits>
 
 #include "common.hpp"
@@ -36,70 +46,97 @@ struct BwdParams {
   const void* swept;  // [b, d] the other modality
   int64_t b, d;
   const float* scale;
-  const float* lse_own;    // [b]
-  const float* lse_swept;  // [b]
-  const float* ell_own;    // [b]  r_i - x_ii of the own side
-  const float* ell_swept;  // [b]
-  const float* udiag;      // [b]  <img_i, txt_i>
-  const float* dloss;      // device scalar or nullptr (= 1)
-  float* dOwn;             // [b, d]
-  double* ds_part;         // [gridDim.x]
+  const float* lse_own;     // [b]  natural-log log-sum-exp of the own side
+  const float* lse2_swept;  // [b]  log-sum-exp of the swept side times log2(e)
+  const float* ell_own;     // [b]  r_i - x_ii of the own side
+  const float* ell_swept;   // [b]
+  const float* udiag;       // [b]  <img_i, txt_i>
+  const float* dloss;       // device scalar or nullptr (= 1)
+  float* dOwn;              // [b, d]
+  double* ds_part;          // [gridDim.x]
 };
 
 constexpr int kBwdBM = 128;  // own rows per workgroup (32 per wave)
+constexpr int kBwdBN = 32;   // swept rows per tile
+// Swept tiles sit in LDS segment-blocked: features are cut into segments of
+// 256 bytes (16 chunks of 16 bytes); segment c >> 4 of all 32 rows is one
+// contiguous 8 KiB block, rows 256 bytes apart, so chunk c of row r lives at
+//   kSeg (c >> 4) + kSegRow r + 16 ((c & 15) ^ g(r)).
+constexpr int kSegRow = 256;
+constexpr int kSeg = kBwdBN * kSegRow;
+constexpr int kGpBytes = kBwdBM * kBwdBN * 2;  // one bf16 G' exchange buffer
 
-// LDS read-ahead (steps) of the two products and the number of independent
-// accumulation chains of the first one (build-time tuning knobs).
+// LDS read-ahead (steps) of GEMM1 (build-time tuning knob).
 #ifndef INFCL_BWD_G1_PRE
 #define INFCL_BWD_G1_PRE 4
 #endif
-#ifndef INFCL_BWD_G1_CHAINS
-#define INFCL_BWD_G1_CHAINS 1
-#endif
-#ifndef INFCL_BWD_G2_PRE
-#define INFCL_BWD_G2_PRE 3
-#endif
-constexpr int kBwdBN = 32;   // swept rows per tile
 
-// Chunk swizzle for the swept tile (rows of >= 16 chunks): 16 rows reading one
-// logical chunk, and the 4 rows x 4 chunks of a transposing read, are both
-// spread over all 64 banks.
+// Chunk swizzle of the swept tile: 16 rows reading one logical chunk, and the
+// 4 rows x 4 chunks of a transposing read, are both spread over all 64 banks.
 __device__ __forceinline__ int bwd_g(int r) { return 4 * (r & 3) + ((r >> 2) & 3); }
 // GEMM1 row permutation: MFMA row m loads swept row perm(m) (bits 2 and 3
 // swapped), so that accumulator register 8s+t of lane half h holds swept row
 // 16s + 8h + t -- exactly the contraction slot t of GEMM2 step s.
 __device__ __forceinline__ int bwd_perm(int m) { return (m & 0x13) | ((m & 4) << 1) | ((m & 8) >> 1); }
 
-template <typename TIN, int D, int FB, bool PIPE, int RING>
+// bf16 32x32x16 MFMA accumulating in VGPRs.  The gradient accumulators fill
+// the AGPRs, and the compiler would otherwise place this chain there too and
+// shuttle accumulator blocks between the register files.  Volatile, so that
+// the chain keeps its order with the interleaved DMA instructions.  Hazards
+// inside inline assembly are not checked by the compiler: two wait states
+// precede each MFMA (a VALU write of a source operand, e.g. an operand the
+// compiler restores with v_accvgpr_read, must be two wait states old), and
+// the last MFMA of a chain is followed by the wait states a VALU read of its
+// result needs, inside the same statement so that nothing reads the
+// accumulator earlier.
+__device__ __forceinline__ void mfma_bf16_vgpr(f32x16& acc, const bf16x8& a, const bf16x8& b, bool first,
+                                               bool last) {
+  if (first && last)
+    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, 0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3"
+                 : "=&v"(acc) : "v"(a), "v"(b));
+  else if (first)
+    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "v"(b));
+  else if (last)
+    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3"
+                 : "+v"(acc) : "v"(a), "v"(b));
+  else
+    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "v"(b));
+}
+
+template <typename TIN, int D, int FB, bool PIPE>
 __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   constexpr int ES = sizeof(TIN);
-  constexpr int EPC = 16 / ES;          // elements per 16-byte chunk
   constexpr int KS = D / 16;            // 16-wide contraction steps of GEMM1
-  constexpr int CPR = D * ES / 16;      // 16-byte chunks per swept row
-  constexpr int ROWB = CPR * 16;        // bytes per swept row in LDS
-  constexpr int TILEB = kBwdBN * ROWB;  // bytes per swept tile
-  constexpr int NI = TILEB / 1024;      // 1 KiB DMA instructions per tile
-  constexpr int NIW = NI / 4;           // ... per wave
-  constexpr int FP = 32 * FB;           // features per pass
-  constexpr int NPASS = D / FP;
-  // three tile buffers (t in GEMM2, t+1 in GEMM1, t+2 loading) when they fit,
-  // otherwise two (GEMM1 -> G' -> GEMM2 per tile while the next tile loads)
-  // PIPE: three tile buffers (t in GEMM2, t+1 in GEMM1, t+2 loading).
-  // Otherwise a ring of RING buffers: GEMM1 -> G' -> GEMM2 per tile while the
-  // next RING-1 tiles load (clamped to what fits in LDS).
-  constexpr int GPB = ES == 2 ? kBwdBM * kBwdBN * 2 : 0;  // G' exchange buffer bytes
-  constexpr int RINGFIT = (160 * 1024 - 2048 - GPB) / (TILEB + 128);
-  constexpr int NBUF = PIPE ? 3 : (RING < RINGFIT ? RING : RINGFIT);
-  static_assert(NBUF >= 2, "at least two tile buffers");
-  static_assert(D % FP == 0, "pass width must divide d");
-  static_assert(CPR % 16 == 0 && NI % 4 == 0, "rows must hold a multiple of 16 chunks");
-  static_assert(NBUF * (TILEB + 128) + GPB + 2048 <= 160 * 1024, "LDS budget");
-  __shared__ __attribute__((aligned(1024))) char lds_[NBUF * TILEB + NBUF * 128 + GPB];
-  INFCL_LDS char* lds = (INFCL_LDS char*)lds_;
-  INFCL_LDS char* lse_lds = lds + NBUF * TILEB;  // 32 swept log-sum-exp values per buffer
+  constexpr int ROWG = D * ES;          // bytes per row in HBM
+  constexpr int TILEB = kBwdBN * ROWG;  // bytes per swept tile
+  constexpr int NIW = TILEB / 4096;     // 1 KiB DMA instructions per wave and tile
+  constexpr int FBW = ES == 2 ? FB / 4 : FB;  // 32-feature blocks per wave and pass
+  constexpr int NACC = ES == 2 ? 4 * FBW : FB;
+  constexpr int NPASS = D / (32 * FB);
+  constexpr int GPN = ES == 2 ? (PIPE ? 2 : 1) : 0;  // G' exchange buffers
+  static_assert(!PIPE || ES == 2, "the pipelined schedule is bf16 only");
+  static_assert(D % (32 * FB) == 0, "pass width must divide d");
+  static_assert(ES == 4 || FB % 4 == 0, "bf16 pass width is a multiple of 128 features");
+  static_assert(D % 64 == 0 && KS % NIW == 0, "tile DMA layout");
+  static_assert((PIPE ? 3 : 2) * (TILEB + 128) + GPN * kGpBytes + 2048 <= 160 * 1024, "LDS budget");
+  __shared__ __attribute__((aligned(1024))) char tA_[TILEB];
+  __shared__ __attribute__((aligned(1024))) char tB_[TILEB];
+  __shared__ __attribute__((aligned(1024))) char tC_[PIPE ? TILEB : 16];
+  __shared__ __attribute__((aligned(16))) float lA_[kBwdBN];
+  __shared__ __attribute__((aligned(16))) float lB_[kBwdBN];
+  __shared__ __attribute__((aligned(16))) float lC_[kBwdBN];
+  __shared__ __attribute__((aligned(1024))) char gp_[GPN ? GPN * kGpBytes : 16];
+  __shared__ double red[256];
+  INFCL_LDS char* const tA = (INFCL_LDS char*)tA_;
+  INFCL_LDS char* const tB = (INFCL_LDS char*)tB_;
+  INFCL_LDS char* const tC = (INFCL_LDS char*)tC_;
+  INFCL_LDS float* const lA = (INFCL_LDS float*)lA_;
+  INFCL_LDS float* const lB = (INFCL_LDS float*)lB_;
+  INFCL_LDS float* const lC = (INFCL_LDS float*)lC_;
+  INFCL_LDS char* const gp = (INFCL_LDS char*)gp_;
 
   const int lane = __lane_id();
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
   const int l32 = lane & 31, h = lane >> 5;
   const int64_t b = p.b;
   const int64_t own0 = (int64_t)blockIdx.x * kBwdBM + 32 * wave;  // this wave's first own row
@@ -129,35 +166,48 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   const float uO = own_ok ? p.udiag[iown] : 0.f;
   const float gdiag = own_ok ? expm1f(-p.ell_own[iown]) + expm1f(-p.ell_swept[iown]) : 0.f;
 
-  // ---- DMA of a swept tile: instruction k = wave + 4 kk writes LDS bytes
-  // [1024 k, 1024 k + 1024) of the buffer; lane L fills physical chunk 64 k + L,
-  // i.e. row r = (64 k + L) / CPR, physical chunk pc = (64 k + L) % CPR, which
-  // holds logical chunk pc ^ g(r).  The per-lane source offsets are recomputed
-  // at every issue from an opaque copy of the lane id: hoisted out of the loop
-  // they would be spilled, and a scratch reload waits for all in-flight DMA.
-  auto issue_tile = [&](int jt, int buf) {
-    const int64_t j0 = (int64_t)jt * kBwdBN;
-    INFCL_LDS char* dst = lds + buf * TILEB;
+  auto opaque_lane = [&]() {
     int lo = lane;
     asm volatile("" : "+v"(lo));
-    // rows past b fall outside the resource and load as zeros (their G' is masked)
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc((const char*)p.swept + j0 * (D * ES), (b - j0) * (D * ES));
-#pragma unroll
-    for (int kk = 0; kk < NIW; ++kk) {
-      const int F = 64 * (wave + 4 * kk) + lo;
-      const int r = F / CPR, pc = F % CPR;
-      const uint32_t off = (uint32_t)(r * D * ES + (pc ^ bwd_g(r)) * 16);
-      dma16b(rs, (INFCL_LDS void*)(dst + 1024 * (wave + 4 * kk)), off, 0);
-    }
-    if (wave == 0 && lane < 8) {
-      const __amdgpu_buffer_rsrc_t rl = make_rsrc(p.lse_swept + j0, (b - j0) * 4);
-      dma16b(rl, (INFCL_LDS void*)(lse_lds + 128 * buf), 16u * lo, 0);
-    }
+    return lo;
   };
 
-  // ---- per-lane LDS offsets; every read below is one of these plus an
-  // immediate.  They are rebuilt from an opaque lane id inside every tile
-  // iteration (see issue_tile for why nothing lane-dependent may stay live).
+  // ---- DMA of swept tile jt into the segment-blocked layout of dst.
+  // Instruction k = wave + 4 kk fills LDS bytes [1024 k, 1024 k + 1024): segment
+  // k >> 3, rows 4 (k & 7) .. +3; lane L fills row 4 (k & 7) + (L >> 4), physical
+  // chunk L & 15, i.e. logical chunk (L & 15) ^ g(row).  Since g(row) =
+  // 4 (L >> 4) + (k & 3) and k & 3 = wave, the per-lane part of every source
+  // offset is one constant and the rest is wave-uniform.  Lane offsets are
+  // rebuilt from an opaque lane id at each use: a value held across the loop
+  // can be spilled where registers are short, and a scratch reload waits for
+  // all DMA in flight.  Rows past b fall outside the resource and load as
+  // zeros (their G' is masked); jt < 0 loads zeros only.
+  auto dma_lane_off = [&]() {
+    const int lo = opaque_lane();
+    return (uint32_t)((lo >> 4) * ROWG + 16 * ((lo & 15) ^ (4 * (lo >> 4)) ^ wave));
+  };
+  auto dma_kk_off = [&](int kk) {
+    const int k = wave + 4 * kk;
+    return (uint32_t)(4 * (k & 7) * ROWG + 256 * (k >> 3));
+  };
+  auto tile_rsrc = [&](int jt) {
+    const int64_t j0 = (int64_t)(jt < 0 ? 0 : jt) * kBwdBN;
+    return rsrc_words((const char*)p.swept + j0 * ROWG, jt < 0 ? 0 : (b - j0) * ROWG);
+  };
+  auto lse_rsrc = [&](int jt) {
+    const int64_t j0 = (int64_t)(jt < 0 ? 0 : jt) * kBwdBN;
+    return rsrc_words(p.lse2_swept + j0, jt < 0 ? 0 : (b - j0) * 4);
+  };
+  auto issue_tile = [&](int jt, INFCL_LDS char* dst, INFCL_LDS float* ldst) {
+    const u32x4 rs = tile_rsrc(jt);
+    const uint32_t lo = dma_lane_off();
+#pragma unroll
+    for (int kk = 0; kk < NIW; ++kk) dma16_asm(rs, dst + 1024 * (wave + 4 * kk), lo + dma_kk_off(kk));
+    if (wave == 0 && lane < 8) dma16_asm(lse_rsrc(jt), ldst, 16u * (uint32_t)lane);
+  };
+
+  // ---- per-lane LDS offsets of GEMM1's swept fragments; every read is one
+  // of these plus an immediate (rebuilt per tile from an opaque lane id)
   auto make_offA = [&](int lo, int (&offA)[8]) {
     const int l32o = lo & 31, ho = lo >> 5;
     const int rA = bwd_perm(l32o);
@@ -165,67 +215,52 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const int cl = ES == 2 ? (2 * k + ho) : (4 * (k >> 1) + 2 * ho + (k & 1));
-      offA[k] = rA * ROWB + 16 * (cl ^ gA);
+      offA[k] = rA * kSegRow + 16 * (cl ^ gA);
     }
-  };
-  auto make_offT = [&](int lo, int (&offT)[2][4]) {
-    const int g4 = lo >> 4, l16 = lo & 15;
-    const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
-    const int lb = 2 * nb16 + (qq >> 1);
-    const int fo = (qq & 1) * 8;
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int fm = 0; fm < 4; ++fm)
-        offT[t][fm] = (8 * hh + e) * ROWB + 16 * (4 * (fm ^ e) + (lb ^ ((t + 2 * hh) & 3))) + fo;
-  };
-  auto opaque_lane = [&]() {
-    int lo = lane;
-    asm volatile("" : "+v"(lo));
-    return lo;
   };
 
   double ds_acc = 0.0;
 
-  // GEMM1 of swept tile jt (in buffer buf): S^T block, MFMA row m <-> swept row j0 + perm(m).
-  // bf16: LDS fragments are read kPre steps ahead of their MFMA through a
-  // register ring, and the steps alternate between two accumulators so that
-  // consecutive MFMAs are independent; the scheduling groups pin the order
-  // MFMA, read, MFMA, read, ...
-  auto gemm1 = [&](int buf) {
-    const INFCL_LDS char* cur = lds + buf * TILEB;
+  // ---- GEMM1 of the tile in cur: S^T block, MFMA row m <-> swept row perm(m).
+  // LDS fragments are read kPre steps ahead of their MFMA through a register
+  // ring.  With with_dma, the loads of tile dtile into (ddst, dlse) are issued
+  // between the MFMAs, one 1 KiB instruction per KS / NIW steps.
+  auto gemm1 = [&](const INFCL_LDS char* cur, bool with_dma, int dtile, INFCL_LDS char* ddst,
+                   INFCL_LDS float* dlse) {
     int offA[8];
     make_offA(opaque_lane(), offA);
+    u32x4 drs = tile_rsrc(-1), drl = lse_rsrc(-1);
+    uint32_t dlo = 0;
+    if (with_dma) {
+      drs = tile_rsrc(dtile);
+      drl = lse_rsrc(dtile);
+      dlo = dma_lane_off();
+    }
+    auto dma_step = [&](int s2) {
+      if (!with_dma) return;
+      constexpr int SPI = KS / NIW;  // steps per DMA instruction
+      if ((s2 + 1) % SPI == 0) {
+        const int kk = (s2 + 1) / SPI - 1;
+        dma16_asm(drs, ddst + 1024 * (wave + 4 * kk), dlo + dma_kk_off(kk));
+      }
+      if (s2 == (KS > 1 ? 1 : 0) && wave == 0 && lane < 8) dma16_asm(drl, dlse, 16u * (uint32_t)lane);
+    };
     f32x16 sacc;
     if constexpr (ES == 2) {
       constexpr int kPre = KS < INFCL_BWD_G1_PRE ? KS : INFCL_BWD_G1_PRE;
-      constexpr int NCH = INFCL_BWD_G1_CHAINS;
-      f32x16 acc2[NCH];
-#pragma unroll
-      for (int c = 0; c < NCH; ++c)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc2[c][r] = 0.f;
       bf16x8 ring[kPre];
 #pragma unroll
-      for (int i = 0; i < kPre; ++i) ring[i] = *(const INFCL_LDS bf16x8*)(cur + offA[i & 7] + 256 * (i >> 3));
+      for (int i = 0; i < kPre; ++i) ring[i] = *(const INFCL_LDS bf16x8*)(cur + offA[i & 7] + kSeg * (i >> 3));
       __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
 #pragma unroll
       for (int s2 = 0; s2 < KS; ++s2) {
-        const bf16x8 a = ring[s2 % kPre];
-        acc2[s2 % NCH] = mfma_bf16(a, ownf[s2][0], acc2[s2 % NCH]);
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        mfma_bf16_vgpr(sacc, ring[s2 % kPre], ownf[s2][0], s2 == 0, s2 == KS - 1);
+        dma_step(s2);
         if (s2 + kPre < KS) {
           const int n = s2 + kPre;
-          ring[s2 % kPre] = *(const INFCL_LDS bf16x8*)(cur + offA[n & 7] + 256 * (n >> 3));
+          ring[s2 % kPre] = *(const INFCL_LDS bf16x8*)(cur + offA[n & 7] + kSeg * (n >> 3));
           __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
-      }
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float v = acc2[0][r];
-#pragma unroll
-        for (int c = 1; c < NCH; ++c) v += acc2[c][r];
-        sacc[r] = v;
       }
     } else {
 #pragma unroll
@@ -233,45 +268,49 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
 #pragma unroll
       for (int s2 = 0; s2 < KS; ++s2) {
         const int kb = 2 * (s2 & 3);
-        f32x4 a0 = *(const INFCL_LDS f32x4*)(cur + offA[kb] + 256 * (s2 >> 2));
-        f32x4 a1 = *(const INFCL_LDS f32x4*)(cur + offA[kb + 1] + 256 * (s2 >> 2));
+        f32x4 a0 = *(const INFCL_LDS f32x4*)(cur + offA[kb] + kSeg * (s2 >> 2));
+        f32x4 a1 = *(const INFCL_LDS f32x4*)(cur + offA[kb + 1] + kSeg * (s2 >> 2));
 #pragma unroll
         for (int t = 0; t < 4; ++t) sacc = mfma_f32(a0[t], ownf[s2][0][t], sacc);
 #pragma unroll
         for (int t = 0; t < 4; ++t) sacc = mfma_f32(a1[t], ownf[s2][1][t], sacc);
+        dma_step(s2);
       }
     }
     return sacc;
   };
 
-  // G' of swept tile jt from its S^T block (log2 domain); entry r <-> swept row
-  // j = j0 + 16 (r>>3) + 8h + (r&7).  Returns the dscale contribution.
-  auto epilogue = [&](int jt, int buf, const f32x16& sacc, float (&gv)[16]) -> float {
+  // ---- G' of swept tile jt from its S^T block (log2 domain); entry r <->
+  // swept row j = 16 (r>>3) + 8h + (r&7) of the tile.  Returns the dscale
+  // contribution.  Tiles touching the diagonal or the ragged end take the
+  // masked path (uniform branch).
+  auto tile_special = [&](int jt) {
+    const int64_t j0 = (int64_t)jt * kBwdBN;
+    return (j0 == own0) || (j0 + kBwdBN > b) || !wave_rows_ok;
+  };
+  auto epilogue = [&](int jt, const INFCL_LDS float* lsep, const f32x16& sacc, float (&gv)[16]) -> float {
     const int64_t j0 = (int64_t)jt * kBwdBN;
     float ds_tile = 0.f;
-    const bool special = (j0 == own0) || (j0 + kBwdBN > b) || !wave_rows_ok;
-    if (!special) {
-      float aS[16];
-      const INFCL_LDS char* lp = lse_lds + 128 * buf + 32 * (opaque_lane() >> 5);
+    if (!tile_special(jt)) {
+      const INFCL_LDS char* lp = (const INFCL_LDS char*)lsep + 32 * h;
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4) {
         const f32x4 v = *(const INFCL_LDS f32x4*)(lp + 64 * (q4 >> 1) + 16 * (q4 & 1));
 #pragma unroll
-        for (int c = 0; c < 4; ++c) aS[4 * q4 + c] = v[c] * kLog2e;
-      }
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float pO = exp2_hw(__builtin_fmaf(sacc[r], k2, -aO));
-        const float pS = exp2_hw(__builtin_fmaf(sacc[r], k2, -aS[r]));
-        gv[r] = pO + pS;
-        ds_tile = __builtin_fmaf(pO, sacc[r] - uO, ds_tile);
+        for (int c = 0; c < 4; ++c) {
+          const int r = 4 * q4 + c;
+          const float pO = exp2_hw(__builtin_fmaf(sacc[r], k2, -aO));
+          const float pS = exp2_hw(__builtin_fmaf(sacc[r], k2, -v[c]));
+          gv[r] = pO + pS;
+          ds_tile = __builtin_fmaf(pO, sacc[r] - uO, ds_tile);
+        }
       }
     } else {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int64_t j = j0 + 16 * (r >> 3) + 8 * h + (r & 7);
         const bool jok = j < b;
-        const float aSr = p.lse_swept[jok ? j : b - 1] * kLog2e;
+        const float aSr = p.lse2_swept[jok ? j : b - 1];
         const float pO = exp2_hw(__builtin_fmaf(sacc[r], k2, -aO));
         const float pS = exp2_hw(__builtin_fmaf(sacc[r], k2, -aSr));
         const bool ok = own_ok && jok;
@@ -284,66 +323,118 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
     }
     return ds_tile;
   };
+  auto to_bf16 = [](const float (&gv)[16], bf16x8 (&ga)[2]) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) ga[r >> 3][r & 7] = (__bf16)gv[r];
+  };
 
   // G' exchange buffer (bf16): [128 own rows][32 swept rows], 64-byte rows whose
   // four 16-byte chunks are XOR-swizzled by (row >> 2) & 3.
-  constexpr int FBW = ES == 2 ? FB / 4 : FB;  // 32-feature blocks per wave and pass (bf16)
-  INFCL_LDS char* gp_lds = lse_lds + NBUF * 128;
-  auto gp_off = [](int row, int c) { return row * 64 + 16 * (c ^ ((row >> 2) & 3)); };
+  auto put_gp = [&](INFCL_LDS char* gpb, const bf16x8 (&ga)[2]) {
+    const int lo = opaque_lane();
+    const int row = 32 * wave + (lo & 31);
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2)
+      *(INFCL_LDS bf16x8*)(gpb + row * 64 + 16 * ((2 * s2 + (lo >> 5)) ^ ((row >> 2) & 3))) = ga[s2];
+  };
 
   for (int pass = 0; pass < NPASS; ++pass) {
     // bf16: dacc[ob * FBW + fbw] holds own block ob (rows 32 ob .. of the
     // workgroup) x feature block (pass FB + wave FBW + fbw).
     // fp32: dacc[fb] holds this wave's own rows x feature block (pass FB + fb).
-    f32x16 dacc[ES == 2 ? 4 * FBW : FB];
+    f32x16 dacc[NACC];
 #pragma unroll
-    for (int i = 0; i < (ES == 2 ? 4 * FBW : FB); ++i)
+    for (int i = 0; i < NACC; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) dacc[i][r] = 0.f;
 
-    // bf16 GEMM2: every wave multiplies the G' of all four waves (from LDS) by
-    // its quarter of the pass's features of the swept tile (transposing reads).
-    auto gemm2_bf16 = [&](int buf) {
-      const INFCL_LDS char* cur = lds + buf * TILEB;
+    // ---- bf16 GEMM2 of the tile in cur with the G' in gpb, as an explicit
+    // software pipeline over its 2 FBW groups (contraction half s2, feature
+    // block fbw; 4 MFMAs each, one per own block): stage g issues the LDS reads
+    // of group g + 2 and then the MFMAs of group g.  With epi the stages also
+    // compute the G' of the next tile (sacc, log-sum-exp values in lnext), a
+    // share per stage, into ga.  The stages are separate scheduling regions.
+    auto gemm2_staged = [&](bool epi, const INFCL_LDS char* cur, const INFCL_LDS char* gpb,
+                            const INFCL_LDS float* lnext, const f32x16& sacc, bf16x8 (&ga)[2]) -> float {
+      constexpr int NG = 2 * FBW;
+      constexpr int PD = 2;
+      constexpr int EPS = (16 + NG - 1) / NG;  // G' entries per stage
+      constexpr int NL = EPS > 2 ? 4 : 2;      // live log-sum-exp blocks
       const int lo = opaque_lane();
       const int l32o = lo & 31, ho = lo >> 5;
       const int g4 = lo >> 4, l16 = lo & 15;
       const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
       const int lb = 2 * nb16 + (qq >> 1);
       const int fo = (qq & 1) * 8;
-      // B-fragment offsets of this wave's feature blocks (read t = 0, 1)
-      int offB[2][FBW];
+      const int gpo = l32o * 64;  // G' row of own block 0; own block ob adds 2048 ob
+      const int gsw = (l32o >> 2) & 3;
+      const INFCL_LDS char* lp = (const INFCL_LDS char*)lnext + 32 * ho;
+      auto readL = [&](int q4) { return *(const INFCL_LDS f32x4*)(lp + 64 * (q4 >> 1) + 16 * (q4 & 1)); };
+      auto first_stage = [](int q) { return (4 * q) / EPS; };  // first stage using LSE block q
+      auto readA = [&](int s2, bf16x8 (&A)[4]) {
 #pragma unroll
-      for (int fbw = 0; fbw < FBW; ++fbw) {
+        for (int ob = 0; ob < 4; ++ob)
+          A[ob] = *(const INFCL_LDS bf16x8*)(gpb + 2048 * ob + gpo + 16 * ((2 * s2 + ho) ^ gsw));
+      };
+      auto readB = [&](int g, s16x4 (&bq)[2]) {
+        const int s2 = g / FBW, fbw = g % FBW;
         const int fbabs = pass * FB + wave * FBW + fbw;
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
-          offB[t][fbw] = (8 * hh + 4 * t + e) * ROWB +
-                         16 * (16 * (fbabs >> 2) + 4 * ((fbabs & 3) ^ e) + (lb ^ ((t + 2 * hh) & 3))) + fo;
-      }
-      typedef short s16x8 __attribute__((ext_vector_type(8)));
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
-        bf16x8 A[4];
-#pragma unroll
-        for (int ob = 0; ob < 4; ++ob) A[ob] = *(const INFCL_LDS bf16x8*)(gp_lds + gp_off(32 * ob + l32o, 2 * s2 + ho));
-#pragma unroll
-        for (int fbw = 0; fbw < FBW; ++fbw) {
-          const int imm = 16 * s2 * ROWB;
-          s16x4 b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFCL_LDS s16x4*)(cur + offB[0][fbw] + imm));
-          s16x4 b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFCL_LDS s16x4*)(cur + offB[1][fbw] + imm));
-          const s16x8 bb = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
-#pragma unroll
-          for (int ob = 0; ob < 4; ++ob)
-            dacc[ob * FBW + fbw] = mfma_bf16(A[ob], __builtin_bit_cast(bf16x8, bb), dacc[ob * FBW + fbw]);
+        for (int t = 0; t < 2; ++t) {
+          const int off = (8 * hh + 4 * t + e + 16 * s2) * kSegRow + kSeg * (fbabs >> 2) +
+                          16 * (4 * ((fbabs & 3) ^ e) + (lb ^ ((t + 2 * hh) & 3))) + fo;
+          bq[t] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFCL_LDS s16x4*)(cur + off));
         }
+      };
+      // A holds G' of contraction half 0 until the last stage of that half has
+      // issued its MFMAs, then half 1 (read straight after).
+      bf16x8 A[4];
+      s16x4 Bq[PD + 1][2];
+      f32x4 Lq[NL];
+      readA(0, A);
+      if (epi) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (first_stage(q) == 0) Lq[q % NL] = readL(q);
       }
+#pragma unroll
+      for (int g = 0; g < PD && g < NG; ++g) readB(g, Bq[g]);
+      __builtin_amdgcn_sched_barrier(0);
+      float ds_tile = 0.f;
+#pragma unroll
+      for (int g = 0; g < NG; ++g) {
+        if (g + PD < NG) readB(g + PD, Bq[(g + PD) % (PD + 1)]);
+        if (epi) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (first_stage(q) == g + 1) Lq[q % NL] = readL(q);
+#pragma unroll
+          for (int i = 0; i < EPS; ++i) {
+            const int r = g * EPS + i;
+            if (r < 16) {
+              const float x = sacc[r];
+              const float pO = exp2_hw(__builtin_fmaf(x, k2, -aO));
+              const float pS = exp2_hw(__builtin_fmaf(x, k2, -Lq[(r >> 2) % NL][r & 3]));
+              ga[r >> 3][r & 7] = (__bf16)(pO + pS);
+              ds_tile = __builtin_fmaf(pO, x - uO, ds_tile);
+            }
+          }
+        }
+        const int fbw = g % FBW;
+        const s16x4* bq = Bq[g % (PD + 1)];
+        const s16x8 bb = {bq[0][0], bq[0][1], bq[0][2], bq[0][3], bq[1][0], bq[1][1], bq[1][2], bq[1][3]};
+#pragma unroll
+        for (int ob = 0; ob < 4; ++ob)
+          dacc[ob * FBW + fbw] = mfma_bf16(A[ob], __builtin_bit_cast(bf16x8, bb), dacc[ob * FBW + fbw]);
+        if (g == FBW - 1) readA(1, A);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      return ds_tile;
     };
 
-    // fp32 GEMM2: this wave's own rows x all the pass's features; step r
+    // ---- fp32 GEMM2: this wave's own rows x all the pass's features; step r
     // contracts swept row jr(r, h) of each lane half.
-    auto gemm2_f32 = [&](int buf, const float (&gv)[16]) {
-      const INFCL_LDS char* cur = lds + buf * TILEB;
+    auto gemm2_f32 = [&](const INFCL_LDS char* cur, const float (&gv)[16]) {
 #pragma unroll
       for (int fb = 0; fb < FB; ++fb) {
         const int fbabs = pass * FB + fb;
@@ -351,52 +442,88 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
         for (int r = 0; r < 16; ++r) {
           const int j = bwd_perm(8 * (r >> 2) + 4 * h + (r & 3));
           const int cf = 8 * fbabs + (l32 >> 2);
-          float bv = *(const INFCL_LDS float*)(cur + j * ROWB + 16 * (cf ^ bwd_g(j)) + (l32 & 3) * 4);
+          float bv = *(const INFCL_LDS float*)(cur + kSeg * (cf >> 4) + j * kSegRow + 16 * ((cf & 15) ^ bwd_g(j)) +
+                                               (l32 & 3) * 4);
           dacc[fb] = mfma_f32(gv[r], bv, dacc[fb]);
         }
       }
     };
 
-    // DMA instructions this wave issues per tile (wave 0 also copies the tile's
-    // log-sum-exp values): the wait before a tile's last barrier lets the
-    // NBUF-2 younger tiles stay in flight.
-    for (int k = 0; k < NBUF - 1; ++k)
-      if (k < ntile) issue_tile(k, k);
-    wait_dma();
-    __syncthreads();
-    int bcur = 0;
-    for (int jt = 0; jt < ntile; ++jt) {
-      const int bload = bcur == 0 ? NBUF - 1 : bcur - 1;  // buffer of tile jt-1, free since the last barrier
-      if (jt + NBUF - 1 < ntile) issue_tile(jt + NBUF - 1, bload);
-      float gv[16];
-      f32x16 sacc = gemm1(bcur);
-      const float d0 = epilogue(jt, bcur, sacc, gv);
-      if (pass == 0) ds_acc += (double)d0;
-      if constexpr (ES == 2) {
-        // publish this wave's G' rows (bf16): chunk 2 s2 + h of row 32 wave + l32
-        const int lo = opaque_lane();
-        const int rowg = 32 * wave + (lo & 31);
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
-          bf16x8 ga;
-#pragma unroll
-          for (int t = 0; t < 8; ++t) ga[t] = (__bf16)gv[8 * s2 + t];
-          *(INFCL_LDS bf16x8*)(gp_lds + gp_off(rowg, 2 * s2 + (lo >> 5))) = ga;
-        }
-        __syncthreads();
-        gemm2_bf16(bcur);
-      } else {
-        gemm2_f32(bcur, gv);
-      }
-      // tile jt+1 must be in LDS; tiles jt+2 .. jt+NBUF-1 may still load
-      const int younger = (ntile - 1 - (jt + 1)) < (NBUF - 2) ? (ntile - 1 - (jt + 1)) : (NBUF - 2);
-      if (younger <= 0) {
-        wait_dma();
-      } else {
-        wait_dma_allow(younger * (NIW + (wave == 0 ? 1 : 0)));
+    if constexpr (PIPE) {
+      // Software pipeline over tiles: iteration jt runs GEMM1 of tile jt+1
+      // (issuing the loads of tile jt+2), then GEMM2 of tile jt together with
+      // the G' of tile jt+1.  Three tile buffers rotate; G' buffers alternate.
+      // Past the last tile, GEMM1 runs on a stale buffer and the G' step takes
+      // the masked path (tile rows >= b), so it yields zeros.
+      issue_tile(0, tA, lA);
+      issue_tile(ntile > 1 ? 1 : -1, tB, lB);
+      wait_dma();
+      __syncthreads();
+      {
+        const f32x16 sacc = gemm1(tA, false, -1, tC, lC);
+        float gv[16];
+        const float d0 = epilogue(0, lA, sacc, gv);
+        if (pass == 0) ds_acc += (double)d0;
+        bf16x8 ga[2];
+        to_bf16(gv, ga);
+        put_gp(gp, ga);
       }
       __syncthreads();
-      bcur = bcur == NBUF - 1 ? 0 : bcur + 1;
+      auto body = [&](int jt, const INFCL_LDS char* cur, INFCL_LDS char* nxt, const INFCL_LDS float* lnxt,
+                      INFCL_LDS char* fre, INFCL_LDS float* lfre) {
+        const bool next = jt + 1 < ntile;
+        const f32x16 sacc = gemm1(nxt, true, jt + 2 < ntile ? jt + 2 : -1, fre, lfre);
+        __builtin_amdgcn_sched_barrier(0);
+        bf16x8 ga[2];
+        float dn = gemm2_staged(true, cur, gp + (jt & 1) * kGpBytes, lnxt, sacc, ga);
+        __builtin_amdgcn_sched_barrier(0);
+        if (tile_special(jt + 1)) {
+          float gv[16];
+          dn = epilogue(jt + 1, lnxt, sacc, gv);
+          to_bf16(gv, ga);
+        }
+        if (pass == 0 && next) ds_acc += (double)dn;
+        put_gp(gp + ((jt + 1) & 1) * kGpBytes, ga);
+        wait_dma();
+        __syncthreads();
+      };
+      // Unrolled over the buffer rotation without tests in between: a tile
+      // index past the end is a tile of rows past b, fully masked (zero G').
+      for (int jt = 0; jt < ntile; jt += 3) {
+        body(jt, tA, tB, lB, tC, lC);
+        body(jt + 1, tB, tC, lC, tA, lA);
+        body(jt + 2, tC, tA, lA, tB, lB);
+      }
+    } else {
+      // Two tile buffers: GEMM1 of tile jt (issuing the loads of tile jt+1),
+      // G', GEMM2.
+      issue_tile(0, tA, lA);
+      wait_dma();
+      __syncthreads();
+      auto body = [&](int jt, const INFCL_LDS char* cur, const INFCL_LDS float* lcur, INFCL_LDS char* nxt,
+                      INFCL_LDS float* lnxt) {
+        const f32x16 sacc = gemm1(cur, true, jt + 1 < ntile ? jt + 1 : -1, nxt, lnxt);
+        float gv[16];
+        const float d0 = epilogue(jt, lcur, sacc, gv);
+        if (pass == 0) ds_acc += (double)d0;
+        if constexpr (ES == 2) {
+          bf16x8 ga[2];
+          to_bf16(gv, ga);
+          put_gp(gp, ga);
+          __syncthreads();
+          gemm2_staged(false, cur, gp, lcur, sacc, ga);
+        } else {
+          gemm2_f32(cur, gv);
+        }
+        wait_dma();
+        __syncthreads();
+      };
+      // Unrolled over the buffer pair without a test in between: a tile
+      // index past the end is a tile of rows past b, fully masked (zero G').
+      for (int jt = 0; jt < ntile; jt += 2) {
+        body(jt, tA, lA, tB, lB);
+        body(jt + 1, tB, lB, tA, lA);
+      }
     }
 
     // ---- write dOwn: lane holds feature l32 of a 32-feature block, rows 8(r>>2)+4h+(r&3)
@@ -424,10 +551,11 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
           if (wave_rows_ok || row < b) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fb] = kfin * dacc[fb][r];
         }
     }
+    // the next pass reuses the tile buffers
+    __syncthreads();
   }
 
   // ---- dscale partial of this workgroup: fixed-order reduction
-  __shared__ double red[256];
   red[threadIdx.x] = ds_acc;
   __syncthreads();
   for (int w = 128; w > 0; w >>= 1) {
@@ -459,15 +587,13 @@ __global__ void __launch_bounds__(256) dscale_finish(const double* part, int64_t
 // (16 FB registers) fit next to the own operand (d/4 or d/2 registers); for
 // bf16 FB is also a multiple of 4 (see the transposing-read addressing).
 // Build-time tuning knobs: the register budget shared by the own operand and
-// the gradient accumulators, and whether the three-buffer pipeline is used.
+// the gradient accumulators, and whether the three-buffer pipeline is used
+// (bf16 widths whose three tiles fit in LDS).
 #ifndef INFCL_BWD_REG_BUDGET
 #define INFCL_BWD_REG_BUDGET 384
 #endif
 #ifndef INFCL_BWD_PIPE
-#define INFCL_BWD_PIPE 0
-#endif
-#ifndef INFCL_BWD_RING
-#define INFCL_BWD_RING 2
+#define INFCL_BWD_PIPE 1
 #endif
 
 template <typename TIN, int D>
@@ -483,7 +609,9 @@ static int launch_bwd_d(const BwdParams& p, int nwg, hipStream_t stream) {
     return best;
   }();
   static_assert(ES == 4 || FB % 4 == 0, "bf16 pass width must be a multiple of 128 features");
-  hipLaunchKernelGGL((bwd_sweep<TIN, D, FB, INFCL_BWD_PIPE != 0, INFCL_BWD_RING>), dim3(nwg), dim3(256), 0, stream, p);
+  constexpr int TILEB = kBwdBN * D * ES;
+  constexpr bool PIPE = INFCL_BWD_PIPE != 0 && ES == 2 && 3 * (TILEB + 128) + 2 * kGpBytes + 2048 <= 160 * 1024;
+  hipLaunchKernelGGL((bwd_sweep<TIN, D, FB, PIPE>), dim3(nwg), dim3(256), 0, stream, p);
   return hipGetLastError() == hipSuccess ? 0 : 1;
 }
 
@@ -516,10 +644,25 @@ static int launch_bwd_t(const BwdParams& p, int nwg, hipStream_t stream) {
   return 2;
 }
 
+// Log-sum-exp vectors rescaled to base 2 (the swept side is streamed through
+// LDS next to every tile and used as is).
+__global__ void __launch_bounds__(256) lse_to_log2(const float* lse_r, const float* lse_c, float* l2r, float* l2c,
+                                                   int64_t b) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < b) {
+    l2r[i] = lse_r[i] * kLog2e;
+    l2c[i] = lse_c[i] * kLog2e;
+  }
+}
+
 int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale,
                const float* lse_r, const float* lse_c, const float* aux, const float* dloss, float* dimg, float* dtxt,
-               float* dscale, double* ds_part, hipStream_t stream) {
+               float* dscale, float* lse2, double* ds_part, hipStream_t stream) {
   const int nwg = (int)((b + kBwdBM - 1) / kBwdBM);
+  float* l2r = lse2;
+  float* l2c = lse2 + b;
+  hipLaunchKernelGGL(lse_to_log2, dim3((unsigned)((b + 255) / 256)), dim3(256), 0, stream, lse_r, lse_c, l2r, l2c, b);
+  if (hipGetLastError() != hipSuccess) return 1;
   BwdParams p;
   p.b = b;
   p.d = d;
@@ -530,7 +673,7 @@ int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype
   p.own = img;
   p.swept = txt;
   p.lse_own = lse_r;
-  p.lse_swept = lse_c;
+  p.lse2_swept = l2c;
   p.ell_own = aux;
   p.ell_swept = aux + b;
   p.dOwn = dimg;
@@ -541,7 +684,7 @@ int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype
   p.own = txt;
   p.swept = img;
   p.lse_own = lse_c;
-  p.lse_swept = lse_r;
+  p.lse2_swept = l2r;
   p.ell_own = aux + b;
   p.ell_swept = aux;
   p.dOwn = dtxt;

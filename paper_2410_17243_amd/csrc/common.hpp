@@ -23,6 +23,7 @@ typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
 
 #define INFCL_LDS __attribute__((address_space(3)))
 #define INFCL_GLOBAL __attribute__((address_space(1)))
@@ -79,6 +80,30 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, in
 __device__ __forceinline__ void dma16b(__amdgpu_buffer_rsrc_t rs, INFCL_LDS void* lds_base, uint32_t voff,
                                        uint32_t soff) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds_base, 16, voff, soff, 0, 0);
+}
+
+// The same copy issued from inline assembly, with a raw descriptor (see
+// rsrc_words).  The compiler does not see this as a write to LDS, so it never
+// stalls later LDS reads on it: the caller waits for completion explicitly
+// (wait_dma / wait_dma_allow) before the written buffer is read.  m0 holds
+// the wave-uniform LDS base.  The compiler's hazard checks do not look inside
+// inline assembly, and it may restore an operand right before it (an SGPR of
+// the descriptor with v_readlane, the offset with v_accvgpr_read): the five
+// wait states cover a VALU-written SGPR read by a vector memory instruction,
+// which is the longest of those requirements (and the one of m0).
+__device__ __forceinline__ u32x4 rsrc_words(const void* base, int64_t nbytes) {
+  const int64_t n = nbytes < 0 ? 0 : (nbytes > 0xFFFFFFF0ll ? 0xFFFFFFF0ll : nbytes);
+  const uint64_t a = (uint64_t)base;
+  u32x4 r;
+  r[0] = (uint32_t)a;
+  r[1] = (uint32_t)(a >> 32) & 0xFFFFu;  // stride 0
+  r[2] = (uint32_t)n;                    // num_records (bytes)
+  r[3] = 0x00020000u;
+  return r;
+}
+__device__ __forceinline__ void dma16_asm(const u32x4& rs, const INFCL_LDS void* lds_base, uint32_t voff) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds_base);
+  asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff), "s"(rs), "{m0}"(m0v));
 }
 
 // Merge of two base-2 log-sum-exp pairs (R, l) -> (max R, rescaled sum).
