@@ -37,7 +37,10 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=2, help="workload configuration 1..5 (default 2)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-b", type=int, default=12288)
+    ap.add_argument("--cpu-sample-b", type=int, default=24576,
+                    help="batch size of the oracle sample timed on the host (capped at the workload b)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 256 MiB device copy three times (reference for the HBM byte counters)")
     return ap.parse_args()
 
 
@@ -94,6 +97,15 @@ def main():
         sys.exit(2)
     import numpy as np
     import torch
+
+    if a.calibrate_copy:
+        x = torch.empty((256 << 20) // 4, dtype=torch.float32, device="cuda:0").uniform_()
+        y = torch.empty_like(x)
+        for _ in range(3):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration": "device copy", "bytes_per_copy": 256 << 20, "copies": 3}))
+        return
 
     import paper_2410_17243_amd as infcl
     from paper_2410_17243_amd import synth
@@ -168,8 +180,7 @@ def main():
     alg_bwd_launch = 3.0 * entries * d      # half of the 6 b^2 d algorithmic backward flops
     alg_fwd_launch = 2.0 * entries * d
     achieved = alg_bwd_launch / (bwd_launch_ms * 1e-3)
-    workload = (f"symmetric InfoNCE fwd+bwd, b={b} d={d} {dt_name} embeddings, sigma={cfg['sigma']}, "
-                f"s={cfg['scale']} (config {a.config})")
+    workload = f"symmetric InfoNCE forward+backward, b={b} d={d} {dt_name}, sigma={cfg['sigma']}, s={cfg['scale']}"
     src = source_hash("bwd.hip", "common.hpp")
     traffic = load_traffic("bwd_sweep", workload, src)
 

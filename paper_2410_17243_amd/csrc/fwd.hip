@@ -79,12 +79,12 @@ template <typename TIN>
 __device__ __forceinline__ void fwd_stage_dma(const FwdParams& p, const FwdDmaOffsets& o, int64_t i0, int64_t j0,
                                               int st, INFCL_LDS char* buf, int wave) {
   const int64_t b = p.b, rowb = p.d * (int64_t)sizeof(TIN);
-  const __amdgpu_buffer_rsrc_t ri = make_rsrc((const char*)p.img + i0 * rowb, (b - i0) * rowb);
-  const __amdgpu_buffer_rsrc_t rt = make_rsrc((const char*)p.txt + j0 * rowb, (b - j0) * rowb);
+  const u32x4 ri = rsrc_words((const char*)p.img + i0 * rowb, (b - i0) * rowb);
+  const u32x4 rt = rsrc_words((const char*)p.txt + j0 * rowb, (b - j0) * rowb);
   const uint32_t soff = (uint32_t)st * 128u;
 #pragma unroll
   for (int kk = 0; kk < kFwdRows / 8 / 4; ++kk)
-    dma16b(kk < 2 ? ri : rt, (INFCL_LDS void*)(buf + 1024 * (wave + 4 * kk)), o.off[kk], soff);
+    dma16_asm(kk < 2 ? ri : rt, buf + 1024 * (wave + 4 * kk), o.off[kk], soff);
 }
 
 // MFMA work of one K-stage: acc[mb][nb] += S^T block (j block mb, i block nb).
