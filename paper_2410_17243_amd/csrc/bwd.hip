@@ -37,7 +37,7 @@
 // every wave at issue).
 #include <type_traits>
 
-#include "common.hpp"
+#include "sweep.hpp"
 
 namespace infcl {
 
@@ -57,51 +57,13 @@ struct BwdParams {
 };
 
 constexpr int kBwdBM = 128;  // own rows per workgroup (32 per wave)
-constexpr int kBwdBN = 32;   // swept rows per tile
-// Swept tiles sit in LDS segment-blocked: features are cut into segments of
-// 256 bytes (16 chunks of 16 bytes); segment c >> 4 of all 32 rows is one
-// contiguous 8 KiB block, rows 256 bytes apart, so chunk c of row r lives at
-//   kSeg (c >> 4) + kSegRow r + 16 ((c & 15) ^ g(r)).
-constexpr int kSegRow = 256;
-constexpr int kSeg = kBwdBN * kSegRow;
+constexpr int kBwdBN = kSweepBN;  // swept rows per tile
 constexpr int kGpBytes = kBwdBM * kBwdBN * 2;  // one bf16 G' exchange buffer
 
 // LDS read-ahead (steps) of GEMM1 (build-time tuning knob).
 #ifndef INFCL_BWD_G1_PRE
 #define INFCL_BWD_G1_PRE 4
 #endif
-
-// Chunk swizzle of the swept tile: 16 rows reading one logical chunk, and the
-// 4 rows x 4 chunks of a transposing read, are both spread over all 64 banks.
-__device__ __forceinline__ int bwd_g(int r) { return 4 * (r & 3) + ((r >> 2) & 3); }
-// GEMM1 row permutation: MFMA row m loads swept row perm(m) (bits 2 and 3
-// swapped), so that accumulator register 8s+t of lane half h holds swept row
-// 16s + 8h + t -- exactly the contraction slot t of GEMM2 step s.
-__device__ __forceinline__ int bwd_perm(int m) { return (m & 0x13) | ((m & 4) << 1) | ((m & 8) >> 1); }
-
-// bf16 32x32x16 MFMA accumulating in VGPRs.  The gradient accumulators fill
-// the AGPRs, and the compiler would otherwise place this chain there too and
-// shuttle accumulator blocks between the register files.  Volatile, so that
-// the chain keeps its order with the interleaved DMA instructions.  Hazards
-// inside inline assembly are not checked by the compiler: two wait states
-// precede each MFMA (a VALU write of a source operand, e.g. an operand the
-// compiler restores with v_accvgpr_read, must be two wait states old), and
-// the last MFMA of a chain is followed by the wait states a VALU read of its
-// result needs, inside the same statement so that nothing reads the
-// accumulator earlier.
-__device__ __forceinline__ void mfma_bf16_vgpr(f32x16& acc, const bf16x8& a, const bf16x8& b, bool first,
-                                               bool last) {
-  if (first && last)
-    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, 0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3"
-                 : "=&v"(acc) : "v"(a), "v"(b));
-  else if (first)
-    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "v"(b));
-  else if (last)
-    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3"
-                 : "+v"(acc) : "v"(a), "v"(b));
-  else
-    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "v"(b));
-}
 
 template <typename TIN, int D, int FB, bool PIPE>
 __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
@@ -118,13 +80,15 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   static_assert(D % (32 * FB) == 0, "pass width must divide d");
   static_assert(ES == 4 || FB % 4 == 0, "bf16 pass width is a multiple of 128 features");
   static_assert(D % 64 == 0 && KS % NIW == 0, "tile DMA layout");
-  static_assert((PIPE ? 3 : 2) * (TILEB + 128) + GPN * kGpBytes + 2048 <= 160 * 1024, "LDS budget");
+  static_assert((PIPE ? 3 : 2) * TILEB + 3 * 1024 + GPN * kGpBytes + 2048 <= 160 * 1024, "LDS budget");
   __shared__ __attribute__((aligned(1024))) char tA_[TILEB];
   __shared__ __attribute__((aligned(1024))) char tB_[TILEB];
   __shared__ __attribute__((aligned(1024))) char tC_[PIPE ? TILEB : 16];
-  __shared__ __attribute__((aligned(16))) float lA_[kBwdBN];
-  __shared__ __attribute__((aligned(16))) float lB_[kBwdBN];
-  __shared__ __attribute__((aligned(16))) float lC_[kBwdBN];
+  // log-sum-exp slots: 32 values used; the rest of the 1 KiB catches the zeros
+  // that the other lanes of the (branch-free) slot DMA write
+  __shared__ __attribute__((aligned(1024))) float lA_[256];
+  __shared__ __attribute__((aligned(1024))) float lB_[256];
+  __shared__ __attribute__((aligned(1024))) float lC_[256];
   __shared__ __attribute__((aligned(1024))) char gp_[GPN ? GPN * kGpBytes : 16];
   __shared__ double red[256];
   INFCL_LDS char* const tA = (INFCL_LDS char*)tA_;
@@ -182,14 +146,8 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   // can be spilled where registers are short, and a scratch reload waits for
   // all DMA in flight.  Rows past b fall outside the resource and load as
   // zeros (their G' is masked); jt < 0 loads zeros only.
-  auto dma_lane_off = [&]() {
-    const int lo = opaque_lane();
-    return (uint32_t)((lo >> 4) * ROWG + 16 * ((lo & 15) ^ (4 * (lo >> 4)) ^ wave));
-  };
-  auto dma_kk_off = [&](int kk) {
-    const int k = wave + 4 * kk;
-    return (uint32_t)(4 * (k & 7) * ROWG + 256 * (k >> 3));
-  };
+  auto dma_lane_off = [&]() { return sweep_dma_lane_off(opaque_lane(), wave, ROWG); };
+  auto dma_kk_off = [&](int kk) { return sweep_dma_kk_off(kk, wave, ROWG); };
   auto tile_rsrc = [&](int jt) {
     const int64_t j0 = (int64_t)(jt < 0 ? 0 : jt) * kBwdBN;
     return rsrc_words((const char*)p.swept + j0 * ROWG, jt < 0 ? 0 : (b - j0) * ROWG);
@@ -198,20 +156,25 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
     const int64_t j0 = (int64_t)(jt < 0 ? 0 : jt) * kBwdBN;
     return rsrc_words(p.lse2_swept + j0, jt < 0 ? 0 : (b - j0) * 4);
   };
+  // The log-sum-exp slot of a tile is loaded by every wave with the full wave
+  // (no divergent branch in the middle of GEMM1): lanes 8k..8k+7 all fetch the
+  // tile's 32 values, so the 1 KiB slot holds 8 copies (the first is read).
+  // All waves write the same bytes.
+  auto lse_lane_off = [&]() { return 16u * (uint32_t)(opaque_lane() & 7); };
   auto issue_tile = [&](int jt, INFCL_LDS char* dst, INFCL_LDS float* ldst) {
     const u32x4 rs = tile_rsrc(jt);
     const uint32_t lo = dma_lane_off();
 #pragma unroll
     for (int kk = 0; kk < NIW; ++kk) dma16_asm(rs, dst + 1024 * (wave + 4 * kk), lo + dma_kk_off(kk));
-    if (wave == 0 && lane < 8) dma16_asm(lse_rsrc(jt), ldst, 16u * (uint32_t)lane);
+    dma16_asm(lse_rsrc(jt), ldst, lse_lane_off());
   };
 
   // ---- per-lane LDS offsets of GEMM1's swept fragments; every read is one
   // of these plus an immediate (rebuilt per tile from an opaque lane id)
   auto make_offA = [&](int lo, int (&offA)[8]) {
     const int l32o = lo & 31, ho = lo >> 5;
-    const int rA = bwd_perm(l32o);
-    const int gA = bwd_g(rA);
+    const int rA = sweep_perm(l32o);
+    const int gA = sweep_g(rA);
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const int cl = ES == 2 ? (2 * k + ho) : (4 * (k >> 1) + 2 * ho + (k & 1));
@@ -243,7 +206,7 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
         const int kk = (s2 + 1) / SPI - 1;
         dma16_asm(drs, ddst + 1024 * (wave + 4 * kk), dlo + dma_kk_off(kk));
       }
-      if (s2 == (KS > 1 ? 1 : 0) && wave == 0 && lane < 8) dma16_asm(drl, dlse, 16u * (uint32_t)lane);
+      if (s2 == (KS > 1 ? 1 : 0)) dma16_asm(drl, dlse, lse_lane_off());
     };
     f32x16 sacc;
     if constexpr (ES == 2) {
@@ -440,9 +403,9 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
         const int fbabs = pass * FB + fb;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int j = bwd_perm(8 * (r >> 2) + 4 * h + (r & 3));
+          const int j = sweep_perm(8 * (r >> 2) + 4 * h + (r & 3));
           const int cf = 8 * fbabs + (l32 >> 2);
-          float bv = *(const INFCL_LDS float*)(cur + kSeg * (cf >> 4) + j * kSegRow + 16 * ((cf & 15) ^ bwd_g(j)) +
+          float bv = *(const INFCL_LDS float*)(cur + kSeg * (cf >> 4) + j * kSegRow + 16 * ((cf & 15) ^ sweep_g(j)) +
                                                (l32 & 3) * 4);
           dacc[fb] = mfma_f32(gv[r], bv, dacc[fb]);
         }
@@ -476,6 +439,9 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
         __builtin_amdgcn_sched_barrier(0);
         bf16x8 ga[2];
         float dn = gemm2_staged(true, cur, gp + (jt & 1) * kGpBytes, lnxt, sacc, ga);
+        // pin the unmasked G' here: otherwise it is sunk into the not-special
+        // branch below and computed after GEMM2 instead of alongside it
+        asm volatile("" : "+v"(ga[0]), "+v"(ga[1]), "+v"(dn));
         __builtin_amdgcn_sched_barrier(0);
         if (tile_special(jt + 1)) {
           float gv[16];

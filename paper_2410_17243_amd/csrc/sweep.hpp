@@ -1,0 +1,67 @@
+// Swept-tile machinery shared by the forward and backward sweeps (gfx950).
+//
+// A sweep keeps 32 rows per wave of one side ("own") in registers and streams
+// 32-row tiles of the other side ("swept") through LDS.  The tiles sit in LDS
+// segment-blocked: features are cut into segments of 256 bytes (16 chunks of
+// 16 bytes); segment c >> 4 of all 32 rows is one contiguous 8 KiB block, rows
+// 256 bytes apart, so chunk c of row r lives at
+//   kSeg (c >> 4) + kSegRow r + 16 ((c & 15) ^ sweep_g(r)).
+// The layout makes the row-fragment reads (first product) and the transposing
+// reads (second product of the backward) bank-conflict free, and every DMA
+// lane offset a per-wave constant (see sweep_dma_lane_off).
+#pragma once
+
+#include "common.hpp"
+
+namespace infcl {
+
+constexpr int kSweepBN = 32;  // swept rows per tile
+constexpr int kSegRow = 256;
+constexpr int kSeg = kSweepBN * kSegRow;
+
+// Chunk swizzle: 16 rows reading one logical chunk, and the 4 rows x 4 chunks
+// of a transposing read, are both spread over all 64 banks.
+__device__ __forceinline__ int sweep_g(int r) { return 4 * (r & 3) + ((r >> 2) & 3); }
+// Row permutation of the first product: MFMA row m loads swept row perm(m)
+// (bits 2 and 3 swapped), so that accumulator register 8s+t of lane half h
+// holds swept row 16s + 8h + t of the tile.
+__device__ __forceinline__ int sweep_perm(int m) { return (m & 0x13) | ((m & 4) << 1) | ((m & 8) >> 1); }
+
+// DMA of a swept tile: instruction k = wave + 4 kk fills LDS bytes
+// [1024 k, 1024 k + 1024): segment k >> 3, rows 4 (k & 7) .. +3; lane L fills
+// row 4 (k & 7) + (L >> 4), physical chunk L & 15, i.e. logical chunk
+// (L & 15) ^ sweep_g(row).  Since sweep_g(row) = 4 (L >> 4) + (k & 3) and
+// k & 3 = wave, the per-lane part of every source offset is one constant
+// (lane_off) and the rest is wave-uniform (kk_off).  rowg = bytes per row.
+__device__ __forceinline__ uint32_t sweep_dma_lane_off(int lo, int wave, int rowg) {
+  return (uint32_t)((lo >> 4) * rowg + 16 * ((lo & 15) ^ (4 * (lo >> 4)) ^ wave));
+}
+__device__ __forceinline__ uint32_t sweep_dma_kk_off(int kk, int wave, int rowg) {
+  const int k = wave + 4 * kk;
+  return (uint32_t)(4 * (k & 7) * rowg + 256 * (k >> 3));
+}
+
+// bf16 32x32x16 MFMA accumulating in VGPRs (the compiler would place an
+// accumulation chain in AGPRs, which the backward needs for its gradients).
+// Volatile, so that the chain keeps its order with interleaved DMA
+// instructions.  Hazards inside inline assembly are not checked by the
+// compiler: two wait states precede each MFMA (a VALU write of a source
+// operand, e.g. an operand the compiler restores with v_accvgpr_read, must be
+// two wait states old), and the last MFMA of a chain is followed by the wait
+// states a VALU read of its result needs, inside the same statement so that
+// nothing reads the accumulator earlier.
+__device__ __forceinline__ void mfma_bf16_vgpr(f32x16& acc, const bf16x8& a, const bf16x8& b, bool first,
+                                               bool last) {
+  if (first && last)
+    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, 0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3"
+                 : "=&v"(acc) : "v"(a), "v"(b));
+  else if (first)
+    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "v"(b));
+  else if (last)
+    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3"
+                 : "+v"(acc) : "v"(a), "v"(b));
+  else
+    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "v"(b));
+}
+
+}  // namespace infcl
