@@ -9,7 +9,8 @@
 namespace infcl {
 int launch_fwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale, float* loss,
                double* loss64, float* lse_r, float* lse_c, float* aux, char* ws, hipStream_t stream, int Pr, int Pc,
-               float* rowR, float* rowL, float* colR, float* colL, float* udiag, double* partial);
+               float* rowR, float* rowL, float* colR, float* colL, float* udiag, float* ref2, double* partial);
+void fwd2_grid(int64_t b, int* Pr, int* Pc);
 int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale,
                const float* lse_r, const float* lse_c, const float* aux, const float* dloss, float* dimg, float* dtxt,
                float* dscale, float* lse2, double* ds_part, hipStream_t stream);
@@ -22,25 +23,31 @@ constexpr int64_t kMaxB = (int64_t)1 << 30;
 
 struct Layout {
   int Pr, Pc;
-  size_t rowR, rowL, colR, colL, udiag, fwd_part, lse2, bwd_part, total;
+  size_t rowR, rowL, colR, colL, udiag, ref2, fwd_part, lse2, bwd_part, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Forward grid: Pc column groups (one per XCD when there are enough column
-// tiles) times Pr row groups, about two workgroups per compute unit.
+// Forward grid of the streamed-tiles sweep: Pc column groups (one per XCD
+// when there are enough column tiles) times Pr row groups, about two
+// workgroups per compute unit.  The partial-pair regions also hold those of
+// the resident-rows sweep (Pc2 row partials, Pr2 column partials).
 Layout make_layout(int64_t b) {
   Layout L;
   const int64_t nRT = (b + 63) / 64, nCT = (b + 255) / 256;
   L.Pc = (int)(nCT < 8 ? nCT : 8);
   L.Pr = (int)(nRT < 64 ? nRT : 64);
+  int Pr2 = 0, Pc2 = 0;
+  infcl::fwd2_grid(b, &Pr2, &Pc2);
+  const size_t nrow = (size_t)(L.Pc * 4 > Pc2 ? L.Pc * 4 : Pc2), ncol = (size_t)(L.Pr > Pr2 ? L.Pr : Pr2);
   size_t off = 0;
   const size_t fb = (size_t)b * sizeof(float);
-  L.rowR = off; off = align256(off + (size_t)L.Pc * 4 * fb);
-  L.rowL = off; off = align256(off + (size_t)L.Pc * 4 * fb);
-  L.colR = off; off = align256(off + (size_t)L.Pr * fb);
-  L.colL = off; off = align256(off + (size_t)L.Pr * fb);
+  L.rowR = off; off = align256(off + nrow * fb);
+  L.rowL = off; off = align256(off + nrow * fb);
+  L.colR = off; off = align256(off + ncol * fb);
+  L.colL = off; off = align256(off + ncol * fb);
   L.udiag = off; off = align256(off + fb);
+  L.ref2 = off; off = align256(off + fb);
   L.fwd_part = off; off = align256(off + (size_t)((b + 255) / 256) * sizeof(double));
   L.lse2 = off; off = align256(off + 2 * fb);
   L.bwd_part = off; off = align256(off + (size_t)2 * ((b + 127) / 128) * sizeof(double));
@@ -79,7 +86,8 @@ infcl_status infcl_fwd(const void* img, const void* txt, int64_t b, int64_t d, i
   char* ws = (char*)workspace;
   int rc = infcl::launch_fwd(img, txt, b, d, dtype, scale, loss, loss64, lse_r, lse_c, aux, ws, (hipStream_t)stream,
                              L.Pr, L.Pc, (float*)(ws + L.rowR), (float*)(ws + L.rowL), (float*)(ws + L.colR),
-                             (float*)(ws + L.colL), (float*)(ws + L.udiag), (double*)(ws + L.fwd_part));
+                             (float*)(ws + L.colL), (float*)(ws + L.udiag), (float*)(ws + L.ref2),
+                             (double*)(ws + L.fwd_part));
   return rc == 0 ? INFCL_OK : INFCL_ERR_HIP;
 }
 

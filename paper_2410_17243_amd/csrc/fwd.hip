@@ -522,9 +522,14 @@ __global__ void __launch_bounds__(256) sum_partials(const double* part, int64_t 
 }
 
 // ------------------------------------------------------------ host launchers
-int launch_fwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale, float* loss,
-               double* loss64, float* lse_r, float* lse_c, float* aux, char* ws, hipStream_t stream, int Pr, int Pc,
-               float* rowR, float* rowL, float* colR, float* colL, float* udiag, double* partial) {
+bool fwd2_supported(int64_t d, int dtype);
+void fwd2_grid(int64_t b, int* Pr, int* Pc);
+int launch_fwd2(const void* img, const void* txt, int64_t b, int64_t d, const float* scale, float* rowR, float* rowL,
+                float* colR, float* colL, float* udiag, float* ref2, hipStream_t stream);
+
+static int launch_fwd1(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale,
+                       hipStream_t stream, int Pr, int Pc, float* rowR, float* rowL, float* colR, float* colL,
+                       float* udiag) {
   FwdParams p;
   p.img = img;
   p.txt = txt;
@@ -545,17 +550,21 @@ int launch_fwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype
     hipLaunchKernelGGL(fwd_sweep<__bf16>, grid, dim3(256), 0, stream, p);
   else
     hipLaunchKernelGGL(fwd_sweep<float>, grid, dim3(256), 0, stream, p);
-  if (hipGetLastError() != hipSuccess) return 1;
+  return hipGetLastError() == hipSuccess ? 0 : 1;
+}
 
+static int launch_finalize(int64_t b, const float* scale, float* loss, double* loss64, float* lse_r, float* lse_c,
+                           float* aux, const float* rowR, const float* rowL, int nrowpart, const float* colR,
+                           const float* colL, int ncolpart, const float* udiag, double* partial, hipStream_t stream) {
   FinParams f;
   f.b = b;
   f.scale = scale;
   f.rowR = rowR;
   f.rowL = rowL;
-  f.nrowpart = Pc * 4;
+  f.nrowpart = nrowpart;
   f.colR = colR;
   f.colL = colL;
-  f.ncolpart = Pr;
+  f.ncolpart = ncolpart;
   f.udiag = udiag;
   f.lse_r = lse_r;
   f.lse_c = lse_c;
@@ -566,9 +575,30 @@ int launch_fwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype
   if (hipGetLastError() != hipSuccess) return 1;
   hipLaunchKernelGGL(sum_partials, dim3(1), dim3(256), 0, stream, (const double*)partial, (int64_t)nfin,
                      1.0 / (2.0 * (double)b), loss, loss64);
-  if (hipGetLastError() != hipSuccess) return 1;
+  return hipGetLastError() == hipSuccess ? 0 : 1;
+}
+
+// Forward: bf16 with d <= 512 takes the resident-rows sweep, everything else
+// the streamed-tiles sweep above; both leave partial pairs that the finalize
+// merges.
+int launch_fwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale, float* loss,
+               double* loss64, float* lse_r, float* lse_c, float* aux, char* ws, hipStream_t stream, int Pr, int Pc,
+               float* rowR, float* rowL, float* colR, float* colL, float* udiag, float* ref2, double* partial) {
   (void)ws;
-  return 0;
+  int nrowpart = Pc * 4, ncolpart = Pr;
+  if (fwd2_supported(d, dtype)) {
+    int Pr2 = 0, Pc2 = 0;
+    fwd2_grid(b, &Pr2, &Pc2);
+    const int rc = launch_fwd2(img, txt, b, d, scale, rowR, rowL, colR, colL, udiag, ref2, stream);
+    if (rc != 0) return rc;
+    nrowpart = Pc2;
+    ncolpart = Pr2;
+  } else {
+    const int rc = launch_fwd1(img, txt, b, d, dtype, scale, stream, Pr, Pc, rowR, rowL, colR, colL, udiag);
+    if (rc != 0) return rc;
+  }
+  return launch_finalize(b, scale, loss, loss64, lse_r, lse_c, aux, rowR, rowL, nrowpart, colR, colL, ncolpart, udiag,
+                         partial, stream);
 }
 
 }  // namespace infcl

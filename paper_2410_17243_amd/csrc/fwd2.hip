@@ -1,0 +1,478 @@
+// Forward sweep of the tiled symmetric InfoNCE loss with resident own rows
+// (bf16 inputs, d <= 512, gfx950).
+//
+// What is computed (Sec. 3.1, Eq. 2-5; the in-GPU forward of Sec. 3.2,
+// Alg. 2): the off-diagonal log-sum-exp of every row i and every column j of
+// S = s * img * txt^T, without storing S.
+//
+// Work decomposition.  Workgroup (q, g) of a P_r x P_c grid owns row blocks
+// q, q + P_r, ... of 128 image rows (32 per wave, held in registers as the
+// MFMA operand for the whole block, as Alg. 2 keeps its row tile on chip) and
+// sweeps the text tiles of column group g (32 rows each, streamed through LDS
+// by DMA in the swept-tile layout).  Each tile is one 32 x 32 block of S^T per
+// wave.  Only text tiles move: 32 KiB of DMA per tile and workgroup for
+// 4.2 MFLOP at d = 512.  g = blockIdx mod P_c, so with P_c = 8 the workgroups
+// of a column group share one XCD and its L2.
+//
+// Statistics.  Log-sum-exp values are kept in base 2 as running pairs (R, l)
+// meaning log2(l) + R; the empty sum is l = 0 with any finite R.  New values y
+// are added lazily as exp2(y - R) against a reference R that starts at the
+// diagonal value y_ii = s log2(e) <img_i, txt_i> of the row or column
+// (computed before the sweep; the diagonal itself is excluded from the sums).
+// A tile's addition is accepted while the partial sum stays at most 2^64 and
+// the running sum at least 2^-64 (so that no entry that matters underflows);
+// otherwise the tile is redone exactly: the old pair is normalised to
+// (R + log2 l, 1) and merged with the tile's max-rescaled sum.
+//  - Rows: every lane accumulates its own row over the 16 entries it holds;
+//    the two lane halves merge at the end of the row block into the group's
+//    slot rowR/rowL[g].
+//  - Columns: every column of a tile gets one partial pair per wave (a sum
+//    over its 32 rows, reduced across lanes) against the running pair
+//    colR/colL[q][j] of the workgroup; a wave whose partial fails the bounds
+//    takes its own column maxima as references instead.  The four wave pairs
+//    meet in LDS, and lanes 0..7 of each wave merge them into the running
+//    pairs of 8 columns during the next tile's GEMM1.
+//  The running column pairs of a tile come into LDS with the tile's DMA, so
+//  the sweep makes no other loads, and (as in the backward sweep) the DMA is
+//  issued from inline assembly, so the compiler never waits for it before
+//  unrelated LDS reads.
+#include "sweep.hpp"
+
+namespace infcl {
+
+struct Fwd2Params {
+  const __bf16* img;  // own rows i, [b, d]
+  const __bf16* txt;  // swept rows j, [b, d]
+  int64_t b;
+  const float* scale;
+  const float* ref2;  // [b]  s log2(e) <img_i, txt_i>
+  float* rowR;        // [Pc][b]
+  float* rowL;
+  float* colR;  // [Pr][b]
+  float* colL;
+  int Pr, Pc;
+  int nRB;  // row blocks of 128
+  int nCT;  // column tiles of 32
+};
+
+constexpr int kF2BM = 128;
+constexpr float kTinyBound = 5.421010862427522e-20f;  // 2^-64
+// Widest spread (log2 units) between the wave reference and a row or column
+// reference for which the factorised column pass keeps every entry that
+// matters: a lost term is below 2^-(126 - kWide) of its column reference.
+constexpr float kWide = 30.f;
+
+// <img_i, txt_i> in fp32 and its base-2 scaled value; 8 lanes per row.
+__global__ void __launch_bounds__(256) fwd2_diag(const __bf16* img, const __bf16* txt, int64_t b, int64_t d,
+                                                 const float* scale, float* udiag, float* ref2) {
+  const int64_t i = (int64_t)blockIdx.x * 32 + (threadIdx.x >> 3);
+  const int l8 = threadIdx.x & 7;
+  float acc = 0.f;
+  if (i < b) {
+    const bf16x8* a = (const bf16x8*)(img + i * d);
+    const bf16x8* t = (const bf16x8*)(txt + i * d);
+    for (int64_t c = l8; c < d / 8; c += 8) {
+      const bf16x8 x = a[c], y = t[c];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc = __builtin_fmaf((float)x[e], (float)y[e], acc);
+    }
+  }
+  acc += shfl_xor(acc, 1);
+  acc += shfl_xor(acc, 2);
+  acc += shfl_xor(acc, 4);
+  if (i < b && l8 == 0) {
+    udiag[i] = acc;
+    ref2[i] = acc * (scale[0] * kLog2e);
+  }
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+// Lane of a 32-lane half that ends with value index i in rs16_sum.
+__device__ __forceinline__ int rs16_index(int lane) {
+  return 8 * ((lane >> 4) & 1) + 4 * ((lane >> 3) & 1) + 2 * ((lane >> 2) & 1) + ((lane >> 1) & 1);
+}
+// Reduce-scatter (sum, or max when kMax) over the 32 lanes of each wave half
+// for 16 values, without LDS traffic: on exit lane l holds the total of value
+// index rs16_index(l) (lanes l and l ^ 1 alike).  Lanes l and l ^ 16 pair up
+// through permlane16_swap, then l ^ 8 (row rotate by 8), l ^ 7 (half-row
+// mirror), l ^ 3 and l ^ 1 (quad permutes) through DPP.
+template <bool kMax>
+__device__ __forceinline__ float rs16_op(float a, float b) {
+  return kMax ? fmaxf(a, b) : a + b;
+}
+template <bool kMax>
+__device__ __forceinline__ float rs16(float (&v)[16], int lane) {
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    // even rows keep v[t] and receive the odd rows' v[t]; odd rows keep v[t+8]
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[t]), __float_as_uint(v[t + 8]), false, false);
+    v[t] = rs16_op<kMax>(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  }
+  const bool b3 = (lane & 8) != 0, b2 = (lane & 4) != 0, b1 = (lane & 2) != 0;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const float send = b3 ? v[t] : v[t + 4], keep = b3 ? v[t + 4] : v[t];
+    v[t] = rs16_op<kMax>(keep, dpp_f<0x128>(send));  // row_ror:8
+  }
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const float send = b2 ? v[t] : v[t + 2], keep = b2 ? v[t + 2] : v[t];
+    v[t] = rs16_op<kMax>(keep, dpp_f<0x141>(send));  // row_half_mirror
+  }
+  {
+    const float send = b1 ? v[0] : v[1], keep = b1 ? v[1] : v[0];
+    v[0] = rs16_op<kMax>(keep, dpp_f<0x1B>(send));  // quad_perm [3,2,1,0]
+  }
+  return rs16_op<kMax>(v[0], dpp_f<0xB1>(v[0]));  // quad_perm [1,0,3,2]
+}
+
+// The pair (R, l) as one reference: R + log2 l, or -inf when empty.
+__device__ __forceinline__ float pair_level(float R, float l) {
+  return l > 0.f ? R + __builtin_amdgcn_logf(l) : -__builtin_inff();
+}
+
+template <int D>
+__global__ void __launch_bounds__(256, 2) fwd_sweep2(Fwd2Params p) {
+  constexpr int KS = D / 16;
+  constexpr int ROWG = D * 2;
+  constexpr int TILEB = kSweepBN * ROWG;
+  constexpr int NIW = TILEB / 4096;
+  constexpr int kPre = KS < 4 ? KS : 4;
+  static_assert(D % 64 == 0 && D <= 512 && KS % NIW == 0, "tile DMA layout");
+  static_assert(2 * (2 * TILEB + 4 * 1024 + 5 * 512) <= 160 * 1024, "two workgroups per CU");
+  __shared__ __attribute__((aligned(1024))) char tA_[TILEB];
+  __shared__ __attribute__((aligned(1024))) char tB_[TILEB];
+  // running pairs of the tile's 32 columns: R at [0, 256), l at [256, 512);
+  // the DMA writes 8 copies of each 32-float row
+  __shared__ __attribute__((aligned(1024))) float sA_[512];
+  __shared__ __attribute__((aligned(1024))) float sB_[512];
+  // per tile parity, column and wave: the wave's partial pair (reference, sum)
+  __shared__ __attribute__((aligned(16))) float cxR_[2][32][4];
+  __shared__ __attribute__((aligned(16))) float cxS_[2][32][4];
+  __shared__ __attribute__((aligned(16))) float cw_[4][32];  // per wave: column maxima (bounds-failure path)
+  INFCL_LDS char* const tA = (INFCL_LDS char*)tA_;
+  INFCL_LDS char* const tB = (INFCL_LDS char*)tB_;
+  INFCL_LDS float* const sA = (INFCL_LDS float*)sA_;
+  INFCL_LDS float* const sB = (INFCL_LDS float*)sB_;
+
+  const int lane = __lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int l32 = lane & 31, h = lane >> 5;
+  const int b = (int)p.b;  // at most 2^30
+  const int g = blockIdx.x % p.Pc;
+  const int q = blockIdx.x / p.Pc;
+  const int ct_lo = (int)(((uint32_t)g * (uint32_t)p.nCT) / (uint32_t)p.Pc);
+  const int ct_hi = (int)(((uint32_t)(g + 1) * (uint32_t)p.nCT) / (uint32_t)p.Pc);
+  if (ct_hi <= ct_lo || q >= p.nRB) return;  // uniform over the workgroup
+  const float k2 = p.scale[0] * kLog2e;
+  const float ninf = -__builtin_inff();
+  float* const cR = p.colR + (int64_t)q * b;
+  float* const cL = p.colL + (int64_t)q * b;
+
+  auto opaque_lane = [&]() {
+    int lo = lane;
+    asm volatile("" : "+v"(lo));
+    return lo;
+  };
+  // swept row (tile-relative) of accumulator entry r of this lane
+  auto jrow = [&](int r) { return 16 * (r >> 3) + 8 * h + (r & 7); };
+  auto tile_rsrc = [&](int jt) {
+    const int j0 = (jt < 0 ? 0 : jt) * kSweepBN;
+    return rsrc_words((const char*)p.txt + (int64_t)j0 * ROWG, jt < 0 ? 0 : (int64_t)(b - j0) * ROWG);
+  };
+  // running column pairs of tile jt into slot: on a workgroup's first row
+  // block the reference is the diagonal value and the sum empty (a resource
+  // of zero bytes loads zeros)
+  auto issue_slot = [&](int jt, bool first_rb, INFCL_LDS float* slot) {
+    const int j0 = (jt < 0 ? 0 : jt) * kSweepBN;
+    const int nb = jt < 0 ? 0 : (b - j0) * 4;
+    const uint32_t so = 16u * (uint32_t)(opaque_lane() & 7);
+    dma16_asm(rsrc_words(first_rb ? p.ref2 + j0 : cR + j0, nb), slot, so);
+    dma16_asm(rsrc_words(cL + j0, first_rb ? 0 : nb), slot + 256, so);
+  };
+
+  for (int rb = q; rb < p.nRB; rb += p.Pr) {
+    const bool first_rb = rb == q;
+    const int own0 = rb * kF2BM + 32 * wave;
+    const int iown = own0 + l32;
+    const bool own_ok = iown < b;
+    const int irow = own_ok ? iown : b - 1;
+    const bool wave_rows_ok = own0 + 32 <= b;
+    const bool wave_any_row = own0 < b;
+
+    bf16x8 ownf[KS];
+    {
+      const __bf16* src = p.img + (int64_t)irow * D + 8 * h;
+#pragma unroll
+      for (int s2 = 0; s2 < KS; ++s2) ownf[s2] = *(const bf16x8*)(src + 16 * s2);
+    }
+    float rowR = p.ref2[irow], rowL = 0.f;  // this lane's pair for its row over its half of the columns
+    // wave reference c = max of the wave's row references, alpha = exp2(R_i - c)
+    float cw = 0.f, alpha = 0.f;
+    bool rows_wide = false;
+    auto refresh = [&]() {
+      float m = own_ok ? rowR : ninf;
+#pragma unroll
+      for (int k = 1; k < 64; k <<= 1) m = fmaxf(m, shfl_xor(m, k));
+      cw = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(m == ninf ? 0.f : m)));
+      alpha = own_ok ? exp2_hw(rowR - cw) : 0.f;
+      rows_wide = wave_any(own_ok && rowR < cw - kWide);
+    };
+    refresh();
+
+    {
+      const u32x4 rs = tile_rsrc(ct_lo);
+      const uint32_t lo = sweep_dma_lane_off(opaque_lane(), wave, ROWG);
+#pragma unroll
+      for (int kk = 0; kk < NIW; ++kk) dma16_asm(rs, tA + 1024 * (wave + 4 * kk), lo + sweep_dma_kk_off(kk, wave, ROWG));
+      issue_slot(ct_lo, first_rb, sA);
+    }
+    wait_dma();
+    __syncthreads();
+
+    // one tile: GEMM1 of the tile in cur (issuing the DMA of tile jt+1 into
+    // nxt between its MFMAs), row statistics, column partials, exchange, merge
+    // merge of a tile's column pairs, deferred into the next tile: lanes 0..7
+    // of wave w own columns 8w .. 8w+7 of the tile
+    int pjg = -1;              // global column of the pending merge (-1: none)
+    float pRold = 0.f, pLold = 0.f;
+    const int jc = 8 * wave + (lane & 7);
+    auto merge = [&](const f32x4& r4, const f32x4& s4) {
+      if (lane < 8 && pjg >= 0 && pjg < b) {
+        float R, L;
+        if (r4[0] == pRold && r4[1] == pRold && r4[2] == pRold && r4[3] == pRold) {
+          R = pRold;
+          L = pLold + ((s4[0] + s4[1]) + (s4[2] + s4[3]));
+        } else {
+          // some wave used its own reference: merge the five pairs by level
+          float lv[5];
+          lv[0] = pair_level(pRold, pLold);
+#pragma unroll
+          for (int w = 0; w < 4; ++w) lv[w + 1] = pair_level(r4[w], s4[w]);
+          float M = lv[0];
+#pragma unroll
+          for (int k = 1; k < 5; ++k) M = fmaxf(M, lv[k]);
+          if (M == ninf) {
+            R = pRold;
+            L = 0.f;
+          } else {
+            L = 0.f;
+#pragma unroll
+            for (int k = 0; k < 5; ++k) L += exp2_hw(lv[k] - M);
+            R = M;
+          }
+        }
+        cR[pjg] = R;
+        cL[pjg] = L;
+      }
+    };
+
+    // one tile: GEMM1 of the tile in cur (issuing the DMA of tile jt+1 into
+    // nxt between its MFMAs), the pending merge, row statistics, column
+    // partial pairs into LDS
+    auto body = [&](int jt, const INFCL_LDS char* cur, const INFCL_LDS float* scur, INFCL_LDS char* nxt,
+                    INFCL_LDS float* snxt, int par) {
+      const int j0 = jt * kSweepBN;
+      const int jn = jt + 1 < ct_hi ? jt + 1 : -1;
+      const int ci = rs16_index(lane);
+      const int jl = jrow(ci);  // the column whose partial this lane ends with
+      const float Rmine = scur[jl], Lmine = scur[256 + jl];
+      const float Rold = scur[jc], Lold = scur[256 + jc];
+      const f32x4 pr4 = *(const INFCL_LDS f32x4*)&cxR_[par ^ 1][jc][0];
+      const f32x4 ps4 = *(const INFCL_LDS f32x4*)&cxS_[par ^ 1][jc][0];
+      f32x16 sacc;
+      {
+        int offA[8];
+        {
+          const int lo = opaque_lane();
+          const int rA = sweep_perm(lo & 31);
+          const int gA = sweep_g(rA);
+#pragma unroll
+          for (int k = 0; k < 8; ++k) offA[k] = rA * kSegRow + 16 * ((2 * k + (lo >> 5)) ^ gA);
+        }
+        const u32x4 drs = tile_rsrc(jn);
+        const uint32_t dlo = sweep_dma_lane_off(opaque_lane(), wave, ROWG);
+        bf16x8 ring[kPre];
+#pragma unroll
+        for (int i = 0; i < kPre; ++i) ring[i] = *(const INFCL_LDS bf16x8*)(cur + offA[i & 7] + kSeg * (i >> 3));
+        __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
+#pragma unroll
+        for (int s2 = 0; s2 < KS; ++s2) {
+          mfma_bf16_vgpr(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KS - 1);
+          constexpr int SPI = KS / NIW;  // steps per DMA instruction
+          if ((s2 + 1) % SPI == 0) {
+            const int kk = (s2 + 1) / SPI - 1;
+            dma16_asm(drs, nxt + 1024 * (wave + 4 * kk), dlo + sweep_dma_kk_off(kk, wave, ROWG));
+          }
+          if (s2 == (KS > 1 ? 1 : 0)) issue_slot(jn, first_rb, snxt);
+          if (s2 + kPre < KS) {
+            const int n = s2 + kPre;
+            ring[s2 % kPre] = *(const INFCL_LDS bf16x8*)(cur + offA[n & 7] + kSeg * (n >> 3));
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+        }
+      }
+      merge(pr4, ps4);
+      // entries off the problem or on the diagonal take no part (uniform test)
+      const bool special = (j0 == own0) || (j0 + kSweepBN > b) || !wave_rows_ok;
+      auto keep = [&](int r) {
+        const int j = j0 + jrow(r);
+        return own_ok && j < b && j != iown;
+      };
+      // scaled entry r, -inf when it takes no part
+      auto yv = [&](int r) { return (!special || keep(r)) ? sacc[r] * k2 : ninf; };
+      // ---- row: lazy against its reference, exact when a bound fails
+      float e[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) e[r] = exp2_hw(__builtin_fmaf(sacc[r], k2, -rowR));
+      if (special) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) e[r] = keep(r) ? e[r] : 0.f;
+      }
+      bool rchg = false;
+      {
+        float t = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) t += e[r];
+        const float nl = rowL + t;
+        if (lazy_ok(t) && nl >= kTinyBound) {
+          rowL = nl;
+        } else {
+          float m = ninf;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) m = fmaxf(m, yv(r));
+          const float lev = pair_level(rowR, rowL);
+          const float Rn = fmaxf(lev, m);
+          if (Rn != ninf) {
+            float s = rowL > 0.f ? exp2_hw(lev - Rn) : 0.f;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) s += exp2_hw(yv(r) - Rn);
+            rowR = Rn;
+            rowL = s;
+            rchg = true;
+          }
+        }
+      }
+      // ---- columns: this wave's partial per column against the column's
+      // running reference.  Factorised: exp2(y - R_j) = e * alpha *
+      // exp2(c - R_j) with e = exp2(y - R_i) from the row pass, so one
+      // exponential per entry; when references lie far apart (wide), the
+      // entries are exponentiated against R_j directly.
+      float v[16];
+      float part;
+      if (!wave_any(rows_wide || Rmine < cw - kWide)) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) v[r] = e[r] * alpha;
+        part = rs16<false>(v, lane) * exp2_hw(cw - Rmine);
+      } else {
+        const INFCL_LDS char* sp = (const INFCL_LDS char*)scur + 32 * h;
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const f32x4 r4 = *(const INFCL_LDS f32x4*)(sp + 64 * (q4 >> 1) + 16 * (q4 & 1));
+#pragma unroll
+          for (int c = 0; c < 4; ++c) v[4 * q4 + c] = exp2_hw(yv(4 * q4 + c) - r4[c]);
+        }
+        part = rs16<false>(v, lane);
+      }
+      float Rw = Rmine;
+      const bool mine_bad = !lazy_ok(part) || (Lmine + part < kTinyBound && j0 + jl < b && wave_any_row);
+      if (wave_any(mine_bad)) {
+        // bounds failure: the wave's partial against its own column maxima
+#pragma unroll
+        for (int r = 0; r < 16; ++r) v[r] = yv(r);
+        const float mx = rs16<true>(v, lane);
+        if ((lane & 1) == 0) cw_[wave][jl] = mx;
+        const INFCL_LDS char* mp = (const INFCL_LDS char*)&cw_[wave][0] + 32 * h;
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const f32x4 m4 = *(const INFCL_LDS f32x4*)(mp + 64 * (q4 >> 1) + 16 * (q4 & 1));
+#pragma unroll
+          for (int c = 0; c < 4; ++c) v[4 * q4 + c] = exp2_hw(yv(4 * q4 + c) - (m4[c] == ninf ? 0.f : m4[c]));
+        }
+        const float s2 = rs16<false>(v, lane);
+        Rw = mx == ninf ? Rmine : mx;
+        part = mx == ninf ? 0.f : s2;
+      }
+      if ((lane & 1) == 0) {  // lanes l and l ^ 1 hold the same column
+        cxR_[par][jl][wave] = Rw;
+        cxS_[par][jl][wave] = part;
+      }
+      if (wave_any(rchg)) refresh();
+      pjg = j0 + jc;
+      pRold = Rold;
+      pLold = Lold;
+      wait_dma();  // the next tile and its column pairs are in LDS after the barrier
+      __syncthreads();
+    };
+    for (int jt = ct_lo; jt < ct_hi; jt += 2) {
+      body(jt, tA, sA, tB, sB, 0);
+      if (jt + 1 < ct_hi) body(jt + 1, tB, sB, tA, sA, 1);
+    }
+    {
+      const int lpar = (ct_hi - 1 - ct_lo) & 1;  // parity of the last tile
+      const f32x4 r4 = *(const INFCL_LDS f32x4*)&cxR_[lpar][jc][0];
+      const f32x4 s4 = *(const INFCL_LDS f32x4*)&cxS_[lpar][jc][0];
+      merge(r4, s4);
+    }
+
+    // ---- end of the row block: merge the two lane halves, publish the row pair
+    {
+      float R = rowR, L = rowL;
+      lse2_merge(R, L, shfl_xor(rowR, 32), shfl_xor(rowL, 32));
+      if (h == 0 && own_ok) {
+        p.rowR[(int64_t)g * b + iown] = R;
+        p.rowL[(int64_t)g * b + iown] = L;
+      }
+    }
+    // column pairs stored in this row block are read by the next one's DMA
+    wait_dma();
+    __syncthreads();
+  }
+}
+
+template <int D>
+static int launch_fwd2_d(const Fwd2Params& p, hipStream_t stream) {
+  hipLaunchKernelGGL(fwd_sweep2<D>, dim3(p.Pr * p.Pc), dim3(256), 0, stream, p);
+  return hipGetLastError() == hipSuccess ? 0 : 1;
+}
+
+bool fwd2_supported(int64_t d, int dtype) { return dtype == 0 && (d == 128 || d == 256 || d == 384 || d == 512); }
+
+// Grid of the resident-rows forward for b samples.
+void fwd2_grid(int64_t b, int* Pr, int* Pc) {
+  const int64_t nRB = (b + kF2BM - 1) / kF2BM, nCT = (b + kSweepBN - 1) / kSweepBN;
+  *Pc = (int)(nCT < 8 ? nCT : 8);
+  *Pr = (int)(nRB < 64 ? nRB : 64);
+}
+
+int launch_fwd2(const void* img, const void* txt, int64_t b, int64_t d, const float* scale, float* rowR, float* rowL,
+                float* colR, float* colL, float* udiag, float* ref2, hipStream_t stream) {
+  hipLaunchKernelGGL(fwd2_diag, dim3((unsigned)((b + 31) / 32)), dim3(256), 0, stream, (const __bf16*)img,
+                     (const __bf16*)txt, b, d, scale, udiag, ref2);
+  if (hipGetLastError() != hipSuccess) return 1;
+  Fwd2Params p;
+  p.img = (const __bf16*)img;
+  p.txt = (const __bf16*)txt;
+  p.b = b;
+  p.scale = scale;
+  p.ref2 = ref2;
+  p.rowR = rowR;
+  p.rowL = rowL;
+  p.colR = colR;
+  p.colL = colL;
+  fwd2_grid(b, &p.Pr, &p.Pc);
+  p.nRB = (int)((b + kF2BM - 1) / kF2BM);
+  p.nCT = (int)((b + kSweepBN - 1) / kSweepBN);
+  switch (d) {
+    case 128: return launch_fwd2_d<128>(p, stream);
+    case 256: return launch_fwd2_d<256>(p, stream);
+    case 384: return launch_fwd2_d<384>(p, stream);
+    case 512: return launch_fwd2_d<512>(p, stream);
+  }
+  return 2;
+}
+
+}  // namespace infcl

@@ -64,6 +64,42 @@ def test_scales_bf16(s, sigma):
     _check(gpu, fwd, dI, dT, ds, s32, 512, "bf16")
 
 
+def _case_bits(img, txt, s):
+    """Oracle and GPU on given bf16 bit arrays."""
+    I = synth.as_f64(img, "bf16")
+    T = synth.as_f64(txt, "bf16")
+    s32 = f32_scale(s)
+    fwd, dI, dT, ds = oracle.forward_backward(I, T, s32)
+    return run(img, txt, "bf16", s32), fwd, dI, dT, ds, s32
+
+
+def test_sign_flipped_pairs_bf16():
+    """txt_i = -img_i for a third of the pairs (in runs of 37), s = 100: the
+    diagonal values sit at +-144 in base-2 units, so row and column references
+    lie far apart and far above most entries."""
+    b, d = 1500, 256
+    img, _ = synth.clip_pairs(b, d, 0.3, seed=21, dtype="bf16")
+    txt = img.copy()
+    flip = (np.arange(b) // 37) % 3 == 0
+    txt[flip] ^= np.uint16(0x8000)
+    gpu, fwd, dI, dT, ds, s = _case_bits(img, txt, 100.0)
+    _check(gpu, fwd, dI, dT, ds, s, d, "bf16")
+
+
+def test_mixed_row_norms_bf16():
+    """Rows scaled by 2^-2 .. 2^2 (exact in bf16): entries of one tile spread
+    over a range several times that of unit rows."""
+    b, d = 1300, 384
+    img, txt = synth.clip_pairs(b, d, 1.0, seed=23, dtype="bf16")
+    fi = synth.as_f64(img, "bf16") * (2.0 ** ((np.arange(b) % 5) - 2))[:, None]
+    ft = synth.as_f64(txt, "bf16") * (2.0 ** ((np.arange(b) * 3 % 5) - 2))[:, None]
+    img2 = synth.f32_to_bf16_bits(fi.astype(np.float32))
+    txt2 = synth.f32_to_bf16_bits(ft.astype(np.float32))
+    gpu, fwd, dI, dT, ds, s = _case_bits(img2, txt2, 14.29)
+    # entries reach 16 s in magnitude: the fp32 log-sum-exp bound scales with it
+    _check(gpu, fwd, dI, dT, ds, 16.0 * s, d, "bf16")
+
+
 def test_weak_positive_reading_bf16():
     """Noise added to the unit vector itself: positives barely above the negatives."""
     gpu, fwd, dI, dT, ds, s = _case(1200, 256, 14.29, mode="weak", seed=3)
