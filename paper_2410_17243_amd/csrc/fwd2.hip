@@ -318,12 +318,13 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep2(Fwd2Params p) {
       merge(pr4, ps4);
       // entries off the problem or on the diagonal take no part (uniform test)
       const bool special = (j0 == own0) || (j0 + kSweepBN > b) || !wave_rows_ok;
+      // (bitwise operators: no short-circuit branches)
       auto keep = [&](int r) {
         const int j = j0 + jrow(r);
-        return own_ok && j < b && j != iown;
+        return (bool)(own_ok & (j < b) & (j != iown));
       };
       // scaled entry r, -inf when it takes no part
-      auto yv = [&](int r) { return (!special || keep(r)) ? sacc[r] * k2 : ninf; };
+      auto yv = [&](int r) { return (!special | keep(r)) ? sacc[r] * k2 : ninf; };
       // ---- row: lazy against its reference, exact when a bound fails
       float e[16];
 #pragma unroll
