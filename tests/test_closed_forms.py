@@ -109,3 +109,79 @@ def test_C_periodic_one_hot(b, d, s):
     # (plus 1e-3 of the largest entry for the fp32 exponentials and accumulation).
     assert excess_I <= 1.0 and excess_T <= 1.0
     assert abs(g["dscale"] - ds) <= 2e-2 * abs(ds) + 2.0 ** -120
+
+
+def _device_onehot(b, d):
+    x = torch.zeros(b, d, dtype=torch.bfloat16, device="cuda")
+    i = torch.arange(b, device="cuda")
+    x[i, i % d] = 1.0
+    return x
+
+
+def _check_C_on_device(b, d, s32, f, grads=None):
+    """Closed form C checked on the device, rows in chunks (the full-size
+    matrices stay on the GPU; only maxima come back)."""
+    cls_np = np.arange(d)
+    n = np.bincount(np.arange(b) % d, minlength=d).astype(np.float64)
+    es = math.exp(s32)
+    Zc = n * es + (b - n)
+    loss = math.fsum(n * np.log(n + (b - n) * math.exp(-s32))) / b
+    r_cls = torch.tensor(np.log(Zc), dtype=torch.float64, device="cuda")
+    tol_cls = torch.tensor(lse_tol(s32, d, np.log(Zc)), dtype=torch.float64, device="cuda")
+    assert f["loss64"].item() == pytest.approx(loss, rel=1e-4)
+    idx = torch.arange(b, device="cuda") % d
+    for key in ("lse_r", "lse_c"):
+        err = (f[key].double() - r_cls[idx]).abs() - tol_cls[idx]
+        assert err.max().item() <= 0.0, key
+    if grads is None:
+        return
+    dI, dT, dscale = grads
+    ds_ref = -(1.0 / b) * math.fsum(n * (b - n) / Zc)
+    assert abs(dscale - ds_ref) <= 2e-2 * abs(ds_ref) + 2.0 ** -120
+    # per class c: expected row coef[c] and bound[c] (see _closed_C)
+    coef = np.zeros((d, d))
+    absg = np.zeros((d, d))
+    ell = np.log(n + (b - n) * math.exp(-s32))
+    for c in cls_np:
+        row = n * (1.0 / Zc[c] + 1.0 / Zc) / (2 * b)
+        row[c] = -(b - n[c]) / (b * Zc[c])
+        coef[c] = s32 * row
+        a = n * (1.0 / Zc[c] + 1.0 / Zc)
+        a[c] = (n[c] - 1) * 2 * es / Zc[c] + abs(2 * math.expm1(-ell[c]))
+        absg[c] = a
+    bound = (s32 / (2 * b)) * (2.0 ** -9 * absg + 2.0 ** -120)
+    coef_t = torch.tensor(coef, dtype=torch.float64, device="cuda")
+    slack = torch.tensor(bound + 1e-3 * np.max(np.abs(coef)), dtype=torch.float64, device="cuda")
+    worst = 0.0
+    for g in (dI, dT):
+        for r0 in range(0, b, 65536):
+            r1 = min(b, r0 + 65536)
+            c = torch.arange(r0, r1, device="cuda") % d
+            e = ((g[r0:r1].double() - coef_t[c]).abs() / slack[c]).max().item()
+            worst = max(worst, e)
+    print(f"  closed form C at b={b}: gradient error / bound {worst:.2e}", flush=True)
+    assert worst <= 1.0
+
+
+@pytest.mark.parametrize("b,d,s,with_bwd", [(1048576, 1024, 50.0, True), (4194304, 768, 14.29, False)])
+def test_C_periodic_full_size(b, d, s, with_bwd):
+    """Closed form C at the two largest workloads, inputs built on the device:
+    b = 1M, d = 1024, s = 50 forward and backward; b = 4M, d = 768 forward (its
+    backward takes minutes; the same backward code runs at b = 131072, d = 768
+    above and in the sampled full-size test)."""
+    import paper_2410_17243_amd as infcl
+
+    s32 = f32_scale(s)
+    I = _device_onehot(b, d)
+    T = I.clone()
+    sc = torch.tensor([s32], dtype=torch.float32, device="cuda").reshape(())
+    print(f"closed form C at b={b} d={d} s={s}: forward", flush=True)
+    f = infcl.clip_loss_fwd(I, T, sc)
+    torch.cuda.synchronize()
+    grads = None
+    if with_bwd:
+        print("  backward", flush=True)
+        dI, dT, dscale = infcl.clip_loss_bwd(I, T, sc, f)
+        torch.cuda.synchronize()
+        grads = (dI, dT, float(dscale.item()))
+    _check_C_on_device(b, d, s32, f, grads)
