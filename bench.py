@@ -115,6 +115,14 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
 
+    # the large workloads take seconds to minutes per step: say so on stderr
+    progress = b >= (1 << 17)
+
+    def note(msg):
+        if progress:
+            print(f"[bench config {a.config}] {msg}", file=sys.stderr, flush=True)
+
+    note("generating inputs on the host")
     img_np, txt_np = synth.clip_pairs(b, d, cfg["sigma"], seed=0, dtype=dt_name)
     if dt_name == "bf16":
         img = torch.from_numpy(img_np.view(np.int16)).view(torch.bfloat16).to(dev)
@@ -149,10 +157,12 @@ def main():
         if ev is not None:
             ev[2].record()
 
+    note(f"inputs resident (b={b}, d={d}); first step")
     step()
     torch.cuda.synchronize()
     peak_bytes = torch.cuda.max_memory_allocated(dev)
-    for _ in range(a.warmup):
+    for w in range(a.warmup):
+        note(f"warm-up step {w + 1}/{a.warmup}")
         step()
     torch.cuda.synchronize()
 
@@ -162,6 +172,9 @@ def main():
     t0 = time.perf_counter()
     for k in range(a.steps):
         step(evs[k])
+        if progress:
+            torch.cuda.synchronize()
+            note(f"timed step {k + 1}/{a.steps}: {evs[k][0].elapsed_time(evs[k][2]):.1f} ms")
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     fwd_ms = [e[0].elapsed_time(e[1]) for e in evs]
