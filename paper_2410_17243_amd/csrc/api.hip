@@ -50,7 +50,7 @@ Layout make_layout(int64_t b) {
   L.ref2 = off; off = align256(off + fb);
   L.fwd_part = off; off = align256(off + (size_t)((b + 255) / 256) * sizeof(double));
   L.lse2 = off; off = align256(off + 2 * fb);
-  L.bwd_part = off; off = align256(off + (size_t)2 * ((b + 127) / 128) * sizeof(double));
+  L.bwd_part = off; off = align256(off + (size_t)2 * ((b + 63) / 64) * sizeof(double));  // 64 or 128 rows per WG
   L.total = off;
   return L;
 }

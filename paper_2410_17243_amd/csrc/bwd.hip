@@ -37,27 +37,11 @@
 // every wave at issue).
 #include <type_traits>
 
-#include "sweep.hpp"
+#include "bwd.hpp"
 
 namespace infcl {
 
-struct BwdParams {
-  const void* own;    // [b, d] rows whose gradient this launch produces
-  const void* swept;  // [b, d] the other modality
-  int64_t b, d;
-  const float* scale;
-  const float* lse_own;     // [b]  natural-log log-sum-exp of the own side
-  const float* lse2_swept;  // [b]  log-sum-exp of the swept side times log2(e)
-  const float* ell_own;     // [b]  r_i - x_ii of the own side
-  const float* ell_swept;   // [b]
-  const float* udiag;       // [b]  <img_i, txt_i>
-  const float* dloss;       // device scalar or nullptr (= 1)
-  float* dOwn;              // [b, d]
-  double* ds_part;          // [gridDim.x]
-};
-
 constexpr int kBwdBM = 128;  // own rows per workgroup (32 per wave)
-constexpr int kBwdBN = kSweepBN;  // swept rows per tile
 constexpr int kGpBytes = kBwdBM * kBwdBN * 2;  // one bf16 G' exchange buffer
 
 // LDS read-ahead (steps) of GEMM1 (build-time tuning knob).
@@ -621,10 +605,21 @@ __global__ void __launch_bounds__(256) lse_to_log2(const float* lse_r, const flo
   }
 }
 
+bool bwd_wide_supported(int64_t d, int dtype);
+int bwd_wide_workgroups(int64_t b);
+int launch_bwd_wide(const BwdParams& p, int nwg, hipStream_t stream);
+
+// Backward: bf16 with d = 768 or 1024 takes the single-pass wide-row sweep
+// (64 own rows per workgroup), everything else the 128-row sweep above.
 int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale,
                const float* lse_r, const float* lse_c, const float* aux, const float* dloss, float* dimg, float* dtxt,
                float* dscale, float* lse2, double* ds_part, hipStream_t stream) {
-  const int nwg = (int)((b + kBwdBM - 1) / kBwdBM);
+  const bool wide = bwd_wide_supported(d, dtype);
+  const int nwg = wide ? bwd_wide_workgroups(b) : (int)((b + kBwdBM - 1) / kBwdBM);
+  auto launch = [&](const BwdParams& q) {
+    if (wide) return launch_bwd_wide(q, nwg, stream);
+    return dtype == 0 ? launch_bwd_t<__bf16>(q, nwg, stream) : launch_bwd_t<float>(q, nwg, stream);
+  };
   float* l2r = lse2;
   float* l2c = lse2 + b;
   hipLaunchKernelGGL(lse_to_log2, dim3((unsigned)((b + 255) / 256)), dim3(256), 0, stream, lse_r, lse_c, l2r, l2c, b);
@@ -644,7 +639,7 @@ int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype
   p.ell_swept = aux + b;
   p.dOwn = dimg;
   p.ds_part = ds_part;
-  int rc = dtype == 0 ? launch_bwd_t<__bf16>(p, nwg, stream) : launch_bwd_t<float>(p, nwg, stream);
+  int rc = launch(p);
   if (rc) return rc;
   // launch 2: own = text rows (dtxt), swept = image rows
   p.own = txt;
@@ -655,7 +650,7 @@ int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype
   p.ell_swept = aux;
   p.dOwn = dtxt;
   p.ds_part = ds_part + nwg;
-  rc = dtype == 0 ? launch_bwd_t<__bf16>(p, nwg, stream) : launch_bwd_t<float>(p, nwg, stream);
+  rc = launch(p);
   if (rc) return rc;
   hipLaunchKernelGGL(dscale_finish, dim3(1), dim3(256), 0, stream, (const double*)ds_part, (int64_t)2 * nwg, b,
                      dloss, dscale);

@@ -1,0 +1,25 @@
+// Shared declarations of the backward sweeps (gfx950).
+#pragma once
+
+#include "sweep.hpp"
+
+namespace infcl {
+
+struct BwdParams {
+  const void* own;    // [b, d] rows whose gradient this launch produces
+  const void* swept;  // [b, d] the other modality
+  int64_t b, d;
+  const float* scale;
+  const float* lse_own;     // [b]  natural-log log-sum-exp of the own side
+  const float* lse2_swept;  // [b]  log-sum-exp of the swept side times log2(e)
+  const float* ell_own;     // [b]  r_i - x_ii of the own side
+  const float* ell_swept;   // [b]
+  const float* udiag;       // [b]  <img_i, txt_i>
+  const float* dloss;       // device scalar or nullptr (= 1)
+  float* dOwn;              // [b, d]
+  double* ds_part;          // [gridDim.x]
+};
+
+constexpr int kBwdBN = kSweepBN;  // swept rows per tile
+
+}  // namespace infcl

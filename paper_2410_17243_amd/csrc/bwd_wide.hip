@@ -1,0 +1,299 @@
+// Backward sweep for wide rows (bf16, d = 768 or 1024) in a single pass
+// (gfx950).
+//
+// Same quantities as the 128-row sweep (Sec. 3.1, Eq. 6-8 completed for both
+// halves of the loss and the scale; the appendix's in-GPU backward recomputes
+// every tile from the saved log-sum-exp vectors).  At these widths the
+// gradient accumulators of 128 own rows (128 x d fp32) do not fit the
+// register file, so a workgroup owns 64 rows instead: 64 x d fp32 is 192 or
+// 256 AGPRs per wave.  GEMM1's own operand is then split by contraction: the
+// wave pair (2 ob, 2 ob + 1) holds own block ob (32 rows), each wave one half
+// of the features (d/8 VGPRs), and computes a partial S^T block over its half.
+// Per tile:
+//   GEMM1   partial S^T (32 swept x 32 own) over the wave's feature half,
+//           interleaved with the DMA of the next tile (all four waves);
+//   join    each wave hands the partner the 8 accumulator entries the
+//           partner finishes (LDS), then adds the partner's half of its own 8;
+//   G'      two exp2 per entry for the wave's 8 entries, the diagonal from
+//           expm1 terms, the dscale contribution; bf16 into the shared G'
+//           block (64 own x 32 swept);
+//   GEMM2   each wave multiplies all 64 own rows' G' by its quarter of the
+//           features of the tile (transposing LDS reads), accumulating in
+//           AGPRs.
+// Three barriers per tile (join, G' block, buffer turn-over).
+#include "bwd.hpp"
+
+namespace infcl {
+
+constexpr int kWideBM = 64;  // own rows per workgroup
+
+template <int D>
+__global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
+  constexpr int KS = D / 16;  // 16-wide contraction steps of the full width
+  constexpr int KH = KS / 2;  // steps of one wave (half the features)
+  constexpr int ROWG = D * 2;
+  constexpr int TILEB = kBwdBN * ROWG;
+  constexpr int NIW = TILEB / 4096;  // 1 KiB DMA instructions per wave and tile
+  constexpr int SPI = KH / NIW;      // GEMM1 steps per DMA instruction
+  constexpr int FBW = D / 128;       // 32-feature blocks of GEMM2 per wave
+  constexpr int kPre = 4;
+  static_assert(KH % 8 == 0 && KH % NIW == 0, "feature halves start on a 128-feature segment");
+  static_assert(2 * TILEB + 2 * 1024 + kWideBM * kBwdBN * 2 + 4 * 64 * 32 + 2048 <= 160 * 1024, "LDS budget");
+  __shared__ __attribute__((aligned(1024))) char tA_[TILEB];
+  __shared__ __attribute__((aligned(1024))) char tB_[TILEB];
+  __shared__ __attribute__((aligned(1024))) float lA_[256];
+  __shared__ __attribute__((aligned(1024))) float lB_[256];
+  // G' of the workgroup's 64 own rows for one tile: 64-byte rows (32 swept
+  // rows, bf16) whose four 16-byte chunks are XOR-swizzled by (row >> 2) & 3
+  __shared__ __attribute__((aligned(1024))) char gp_[kWideBM * kBwdBN * 2];
+  // join: per wave and lane the 8 partial entries its partner finishes
+  __shared__ __attribute__((aligned(16))) float xs_[4][64][8];
+  __shared__ double red[256];
+  INFCL_LDS char* const tA = (INFCL_LDS char*)tA_;
+  INFCL_LDS char* const tB = (INFCL_LDS char*)tB_;
+  INFCL_LDS float* const lA = (INFCL_LDS float*)lA_;
+  INFCL_LDS float* const lB = (INFCL_LDS float*)lB_;
+  INFCL_LDS char* const gp = (INFCL_LDS char*)gp_;
+
+  const int lane = __lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int ob = wave >> 1, kh = wave & 1;  // own block, feature half of GEMM1
+  const int l32 = lane & 31, h = lane >> 5;
+  const int64_t b = p.b;
+  const int64_t wg0 = (int64_t)blockIdx.x * kWideBM;
+  const int64_t own0 = wg0 + 32 * ob;  // this wave's own block
+  const int64_t iown = own0 + l32;
+  const bool own_ok = iown < b;
+  const int64_t irow = own_ok ? iown : b - 1;
+  const bool wave_rows_ok = own0 + 32 <= b;
+  const int ntile = (int)((b + kBwdBN - 1) / kBwdBN);
+
+  const float s = p.scale[0];
+  const float k2 = s * kLog2e;
+  const float dl = p.dloss ? p.dloss[0] : 1.0f;
+  const float kfin = dl * s / (2.0f * (float)b);
+
+  // own operand of GEMM1: row irow, features kh d/2 + 16 s2 + 8h .. +8
+  bf16x8 ownf[KH];
+  {
+    const __bf16* src = (const __bf16*)p.own + irow * D + kh * (D / 2) + 8 * h;
+#pragma unroll
+    for (int s2 = 0; s2 < KH; ++s2) ownf[s2] = *(const bf16x8*)(src + 16 * s2);
+  }
+  const float aO = own_ok ? p.lse_own[iown] * kLog2e : 0.f;
+  const float uO = own_ok ? p.udiag[iown] : 0.f;
+  const float gdiag = own_ok ? expm1f(-p.ell_own[iown]) + expm1f(-p.ell_swept[iown]) : 0.f;
+
+  auto opaque_lane = [&]() {
+    int lo = lane;
+    asm volatile("" : "+v"(lo));
+    return lo;
+  };
+  auto tile_rsrc = [&](int jt) {
+    const int64_t j0 = (int64_t)(jt < 0 ? 0 : jt) * kBwdBN;
+    return rsrc_words((const char*)p.swept + j0 * ROWG, jt < 0 ? 0 : (b - j0) * ROWG);
+  };
+  auto lse_rsrc = [&](int jt) {
+    const int64_t j0 = (int64_t)(jt < 0 ? 0 : jt) * kBwdBN;
+    return rsrc_words(p.lse2_swept + j0, jt < 0 ? 0 : (b - j0) * 4);
+  };
+  auto lse_lane_off = [&]() { return 16u * (uint32_t)(opaque_lane() & 7); };
+
+  double ds_acc = 0.0;
+  f32x16 dacc[2 * FBW];
+#pragma unroll
+  for (int i = 0; i < 2 * FBW; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dacc[i][r] = 0.f;
+
+  // ---- GEMM1 over this wave's feature half of the tile in cur; issues the
+  // DMA of tile dtile (all four waves share it) between the MFMAs
+  auto gemm1 = [&](const INFCL_LDS char* cur, int dtile, INFCL_LDS char* ddst, INFCL_LDS float* dlse) {
+    int offA[8];
+    {
+      const int lo = opaque_lane();
+      const int rA = sweep_perm(lo & 31);
+      const int gA = sweep_g(rA);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) offA[k] = rA * kSegRow + 16 * ((2 * k + (lo >> 5)) ^ gA);
+    }
+    const INFCL_LDS char* half = cur + kSeg * (kh * KH / 8);
+    const u32x4 drs = tile_rsrc(dtile);
+    const u32x4 drl = lse_rsrc(dtile);
+    const uint32_t dlo = sweep_dma_lane_off(opaque_lane(), wave, ROWG);
+    f32x16 sacc;
+    bf16x8 ring[kPre];
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) ring[i] = *(const INFCL_LDS bf16x8*)(half + offA[i & 7] + kSeg * (i >> 3));
+    __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
+#pragma unroll
+    for (int s2 = 0; s2 < KH; ++s2) {
+      mfma_bf16_vgpr(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KH - 1);
+      if ((s2 + 1) % SPI == 0) {
+        const int kk = (s2 + 1) / SPI - 1;
+        dma16_asm(drs, ddst + 1024 * (wave + 4 * kk), dlo + sweep_dma_kk_off(kk, wave, ROWG));
+      }
+      if (s2 == 1) dma16_asm(drl, dlse, lse_lane_off());
+      if (s2 + kPre < KH) {
+        const int n = s2 + kPre;
+        ring[s2 % kPre] = *(const INFCL_LDS bf16x8*)(half + offA[n & 7] + kSeg * (n >> 3));
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+    }
+    return sacc;
+  };
+
+  // ---- join, G' of the wave's 8 entries (entry r = 8 kh + i <-> swept row
+  // 16 kh + 8h + i of the tile) into the G' block; returns dscale's share
+  auto join_gp = [&](int jt, const INFCL_LDS float* lcur, const f32x16& sacc) -> float {
+    float mine[8], other[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      mine[i] = kh ? sacc[8 + i] : sacc[i];
+      other[i] = kh ? sacc[i] : sacc[8 + i];
+    }
+    *(INFCL_LDS f32x4*)&xs_[wave][lane][0] = f32x4{other[0], other[1], other[2], other[3]};
+    *(INFCL_LDS f32x4*)&xs_[wave][lane][4] = f32x4{other[4], other[5], other[6], other[7]};
+    __syncthreads();
+    const f32x4 q0 = *(const INFCL_LDS f32x4*)&xs_[wave ^ 1][lane][0];
+    const f32x4 q1 = *(const INFCL_LDS f32x4*)&xs_[wave ^ 1][lane][4];
+    const INFCL_LDS float* lp = lcur + 16 * kh + 8 * h;
+    const f32x4 L0 = *(const INFCL_LDS f32x4*)lp;
+    const f32x4 L1 = *(const INFCL_LDS f32x4*)(lp + 4);
+    const int64_t j0 = (int64_t)jt * kBwdBN;
+    const bool special = (j0 == own0) || (j0 + kBwdBN > b) || !wave_rows_ok;
+    float ds_tile = 0.f;
+    bf16x8 ga;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float x = mine[i] + (i < 4 ? q0[i] : q1[i - 4]);
+      const float Lj = i < 4 ? L0[i] : L1[i - 4];
+      const float pO = exp2_hw(__builtin_fmaf(x, k2, -aO));
+      const float pS = exp2_hw(__builtin_fmaf(x, k2, -Lj));
+      float gg = pO + pS;
+      float dsv = pO * (x - uO);
+      if (special) {
+        const int64_t j = j0 + 16 * kh + 8 * h + i;
+        const bool ok = (bool)(own_ok & (j < b));
+        const bool dg = j == iown;
+        gg = dg ? gdiag : (ok ? gg : 0.f);
+        dsv = (ok & !dg) ? dsv : 0.f;
+      }
+      ds_tile += dsv;
+      ga[i] = (__bf16)gg;
+    }
+    const int row = 32 * ob + l32;
+    *(INFCL_LDS bf16x8*)(gp + row * 64 + 16 * ((2 * kh + h) ^ ((row >> 2) & 3))) = ga;
+    return ds_tile;
+  };
+
+  // ---- GEMM2: all 64 own rows' G' x this wave's quarter of the tile's
+  // features (transposing reads of the segment-blocked tile)
+  auto gemm2 = [&](const INFCL_LDS char* cur) {
+    const int lo = opaque_lane();
+    const int l32o = lo & 31, ho = lo >> 5;
+    const int g4 = lo >> 4, l16 = lo & 15;
+    const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
+    const int lb = 2 * nb16 + (qq >> 1);
+    const int fo = (qq & 1) * 8;
+    const int gpo = l32o * 64;
+    const int gsw = (l32o >> 2) & 3;
+    auto readB = [&](int g, s16x4 (&bq)[2]) {
+      const int s2 = g / FBW, fbabs = wave * FBW + g % FBW;
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int off = (8 * hh + 4 * t + e + 16 * s2) * kSegRow + kSeg * (fbabs >> 2) +
+                        16 * (4 * ((fbabs & 3) ^ e) + (lb ^ ((t + 2 * hh) & 3))) + fo;
+        bq[t] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFCL_LDS s16x4*)(cur + off));
+      }
+    };
+    // one group (contraction half s2, feature block fbw) per stage, the
+    // transposing reads one stage ahead; stages are separate scheduling
+    // regions, which keeps the read-ahead (and the registers) bounded
+    bf16x8 A[2];
+    s16x4 bq[2][2];
+    readB(0, bq[0]);
+#pragma unroll
+    for (int g = 0; g < 2 * FBW; ++g) {
+      const int s2 = g / FBW, fbw = g % FBW;
+      if (fbw == 0) {
+#pragma unroll
+        for (int o2 = 0; o2 < 2; ++o2)
+          A[o2] = *(const INFCL_LDS bf16x8*)(gp + 2048 * o2 + gpo + 16 * ((2 * s2 + ho) ^ gsw));
+      }
+      if (g + 1 < 2 * FBW) readB(g + 1, bq[(g + 1) & 1]);
+      const s16x4* q = bq[g & 1];
+      const s16x8 bb = {q[0][0], q[0][1], q[0][2], q[0][3], q[1][0], q[1][1], q[1][2], q[1][3]};
+#pragma unroll
+      for (int o2 = 0; o2 < 2; ++o2)
+        dacc[o2 * FBW + fbw] = mfma_bf16(A[o2], __builtin_bit_cast(bf16x8, bb), dacc[o2 * FBW + fbw]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  // ---- sweep: tile jt in cur (LSE slot lcur); the DMA of tile jt+1 goes to
+  // nxt during GEMM1
+  auto body = [&](int jt, const INFCL_LDS char* cur, const INFCL_LDS float* lcur, INFCL_LDS char* nxt,
+                  INFCL_LDS float* lnxt) {
+    const f32x16 sacc = gemm1(cur, jt + 1 < ntile ? jt + 1 : -1, nxt, lnxt);
+    ds_acc += (double)join_gp(jt, lcur, sacc);
+    __syncthreads();  // the G' block is complete
+    gemm2(cur);
+    wait_dma();
+    __syncthreads();  // tile jt+1 landed; cur, the G' block and the join area are free
+  };
+  {
+    const u32x4 rs = tile_rsrc(0);
+    const uint32_t lo = sweep_dma_lane_off(opaque_lane(), wave, ROWG);
+#pragma unroll
+    for (int kk = 0; kk < NIW; ++kk) dma16_asm(rs, tA + 1024 * (wave + 4 * kk), lo + sweep_dma_kk_off(kk, wave, ROWG));
+    dma16_asm(lse_rsrc(0), lA, lse_lane_off());
+  }
+  wait_dma();
+  __syncthreads();
+  // one body with the buffers picked per tile (an unrolled pair of bodies
+  // doubles the live ranges and spills at these widths)
+  for (int jt = 0; jt < ntile; ++jt) {
+    const bool odd = (jt & 1) != 0;
+    body(jt, odd ? tB : tA, odd ? lB : lA, odd ? tA : tB, odd ? lA : lB);
+  }
+
+  // ---- write dOwn: accumulator dacc[o2 FBW + fbw] lane holds feature l32 of
+  // block (wave FBW + fbw), rows 8(r>>2) + 4h + (r&3) of own block o2
+  const bool all_ok = wg0 + kWideBM <= b;
+#pragma unroll
+  for (int o2 = 0; o2 < 2; ++o2) {
+    float* dst = p.dOwn + (wg0 + 32 * o2 + 4 * h) * D + 32 * (wave * FBW) + l32;
+#pragma unroll
+    for (int fbw = 0; fbw < FBW; ++fbw)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = wg0 + 32 * o2 + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (all_ok || row < b) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fbw] = kfin * dacc[o2 * FBW + fbw][r];
+      }
+  }
+
+  // ---- dscale partial of this workgroup: fixed-order reduction
+  red[threadIdx.x] = ds_acc;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) p.ds_part[blockIdx.x] = red[0];
+}
+
+bool bwd_wide_supported(int64_t d, int dtype) { return dtype == 0 && (d == 768 || d == 1024); }
+
+int bwd_wide_workgroups(int64_t b) { return (int)((b + kWideBM - 1) / kWideBM); }
+
+int launch_bwd_wide(const BwdParams& p, int nwg, hipStream_t stream) {
+  switch (p.d) {
+    case 768: hipLaunchKernelGGL(bwd_wide<768>, dim3(nwg), dim3(256), 0, stream, p); break;
+    case 1024: hipLaunchKernelGGL(bwd_wide<1024>, dim3(nwg), dim3(256), 0, stream, p); break;
+    default: return 2;
+  }
+  return hipGetLastError() == hipSuccess ? 0 : 1;
+}
+
+}  // namespace infcl
