@@ -55,7 +55,13 @@ struct Fwd2Params {
   int nCT;  // column tiles of 32
 };
 
-constexpr int kF2BM = 128;
+// waves per workgroup: 8 (one workgroup per CU, a text tile loaded once per
+// CU) or 4 (two workgroups per CU)
+#ifndef INFCL_FWD2_WAVES
+#define INFCL_FWD2_WAVES 8
+#endif
+constexpr int kF2NW = INFCL_FWD2_WAVES;
+constexpr int kF2BM = 32 * kF2NW;  // own rows per row block
 constexpr float kTinyBound = 5.421010862427522e-20f;  // 2^-64
 // Widest spread (log2 units) between the wave reference and a row or column
 // reference for which the factorised column pass keeps every entry that
@@ -135,13 +141,14 @@ __device__ __forceinline__ float pair_level(float R, float l) {
 }
 
 template <int D>
-__global__ void __launch_bounds__(256, 2) fwd_sweep2(Fwd2Params p) {
+__global__ void __launch_bounds__(64 * kF2NW, 2) fwd_sweep2(Fwd2Params p) {
+  constexpr int NW = kF2NW;
   constexpr int KS = D / 16;
   constexpr int ROWG = D * 2;
   constexpr int TILEB = kSweepBN * ROWG;
-  constexpr int NIW = TILEB / 4096;
+  constexpr int NIW = TILEB / 1024 / NW;  // 1 KiB DMA instructions per wave and tile
   constexpr int kPre = KS < 4 ? KS : 4;
-  static_assert(D % 64 == 0 && D <= 512 && KS % NIW == 0, "tile DMA layout");
+  static_assert(D % 64 == 0 && D <= 512 && NIW >= 1 && KS % NIW == 0, "tile DMA layout");
   static_assert(2 * (2 * TILEB + 4 * 1024 + 5 * 512) <= 160 * 1024, "two workgroups per CU");
   __shared__ __attribute__((aligned(1024))) char tA_[TILEB];
   __shared__ __attribute__((aligned(1024))) char tB_[TILEB];
@@ -150,9 +157,9 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep2(Fwd2Params p) {
   __shared__ __attribute__((aligned(1024))) float sA_[512];
   __shared__ __attribute__((aligned(1024))) float sB_[512];
   // per tile parity, column and wave: the wave's partial pair (reference, sum)
-  __shared__ __attribute__((aligned(16))) float cxR_[2][32][4];
-  __shared__ __attribute__((aligned(16))) float cxS_[2][32][4];
-  __shared__ __attribute__((aligned(16))) float cw_[4][32];  // per wave: column maxima (bounds-failure path)
+  __shared__ __attribute__((aligned(16))) float cxR_[2][32][NW];
+  __shared__ __attribute__((aligned(16))) float cxS_[2][32][NW];
+  __shared__ __attribute__((aligned(16))) float cw_[NW][32];  // per wave: column maxima (bounds-failure path)
   INFCL_LDS char* const tA = (INFCL_LDS char*)tA_;
   INFCL_LDS char* const tB = (INFCL_LDS char*)tB_;
   INFCL_LDS float* const sA = (INFCL_LDS float*)sA_;
@@ -161,6 +168,11 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep2(Fwd2Params p) {
   const int lane = __lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l32 = lane & 31, h = lane >> 5;
+  // tile DMA: instruction k = wq + 4 kk of the swept-tile layout, kk in [kk0, kk0 + NIW)
+  const int wq = wave & 3, kk0 = (wave >> 2) * NIW;
+  // the running column pairs of a tile are loaded by one wave (8 waves) or,
+  // branch-free, by every wave (4 waves)
+  const bool slot_wave = NW == 4 || wave == 0;
   const int b = (int)p.b;  // at most 2^30
   const int g = blockIdx.x % p.Pc;
   const int q = blockIdx.x / p.Pc;
@@ -225,10 +237,11 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep2(Fwd2Params p) {
 
     {
       const u32x4 rs = tile_rsrc(ct_lo);
-      const uint32_t lo = sweep_dma_lane_off(opaque_lane(), wave, ROWG);
+      const uint32_t lo = sweep_dma_lane_off(opaque_lane(), wq, ROWG);
 #pragma unroll
-      for (int kk = 0; kk < NIW; ++kk) dma16_asm(rs, tA + 1024 * (wave + 4 * kk), lo + sweep_dma_kk_off(kk, wave, ROWG));
-      issue_slot(ct_lo, first_rb, sA);
+      for (int k = 0; k < NIW; ++k)
+        dma16_asm(rs, tA + 1024 * (wq + 4 * (kk0 + k)), lo + sweep_dma_kk_off(kk0 + k, wq, ROWG));
+      if (slot_wave) issue_slot(ct_lo, first_rb, sA);
     }
     wait_dma();
     __syncthreads();
@@ -239,29 +252,49 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep2(Fwd2Params p) {
     // of wave w own columns 8w .. 8w+7 of the tile
     int pjg = -1;              // global column of the pending merge (-1: none)
     float pRold = 0.f, pLold = 0.f;
-    const int jc = 8 * wave + (lane & 7);
-    auto merge = [&](const f32x4& r4, const f32x4& s4) {
-      if (lane < 8 && pjg >= 0 && pjg < b) {
+    const int jc = 8 * wq + (lane & 7);
+    const bool merger = lane < 8 && wave < 4;
+    // the NW wave pairs of column jc of a tile (parity par)
+    auto pairs = [&](int par, float (&rw)[NW], float (&sw)[NW]) {
+#pragma unroll
+      for (int w4 = 0; w4 < NW; w4 += 4) {
+        const f32x4 r4 = *(const INFCL_LDS f32x4*)&cxR_[par][jc][w4];
+        const f32x4 s4 = *(const INFCL_LDS f32x4*)&cxS_[par][jc][w4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          rw[w4 + c] = r4[c];
+          sw[w4 + c] = s4[c];
+        }
+      }
+    };
+    auto merge = [&](const float (&rw)[NW], const float (&sw)[NW]) {
+      if (merger && pjg >= 0 && pjg < b) {
         float R, L;
-        if (r4[0] == pRold && r4[1] == pRold && r4[2] == pRold && r4[3] == pRold) {
+        bool same = true;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) same = same & (rw[w] == pRold);
+        if (same) {
+          float t = 0.f;
+#pragma unroll
+          for (int w = 0; w < NW; ++w) t += sw[w];
           R = pRold;
-          L = pLold + ((s4[0] + s4[1]) + (s4[2] + s4[3]));
+          L = pLold + t;
         } else {
-          // some wave used its own reference: merge the five pairs by level
-          float lv[5];
+          // some wave used its own reference: merge the pairs by level
+          float lv[NW + 1];
           lv[0] = pair_level(pRold, pLold);
 #pragma unroll
-          for (int w = 0; w < 4; ++w) lv[w + 1] = pair_level(r4[w], s4[w]);
+          for (int w = 0; w < NW; ++w) lv[w + 1] = pair_level(rw[w], sw[w]);
           float M = lv[0];
 #pragma unroll
-          for (int k = 1; k < 5; ++k) M = fmaxf(M, lv[k]);
+          for (int k = 1; k <= NW; ++k) M = fmaxf(M, lv[k]);
           if (M == ninf) {
             R = pRold;
             L = 0.f;
           } else {
             L = 0.f;
 #pragma unroll
-            for (int k = 0; k < 5; ++k) L += exp2_hw(lv[k] - M);
+            for (int k = 0; k <= NW; ++k) L += exp2_hw(lv[k] - M);
             R = M;
           }
         }
@@ -281,8 +314,8 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep2(Fwd2Params p) {
       const int jl = jrow(ci);  // the column whose partial this lane ends with
       const float Rmine = scur[jl], Lmine = scur[256 + jl];
       const float Rold = scur[jc], Lold = scur[256 + jc];
-      const f32x4 pr4 = *(const INFCL_LDS f32x4*)&cxR_[par ^ 1][jc][0];
-      const f32x4 ps4 = *(const INFCL_LDS f32x4*)&cxS_[par ^ 1][jc][0];
+      float prw[NW], psw[NW];
+      pairs(par ^ 1, prw, psw);
       f32x16 sacc;
       {
         int offA[8];
@@ -294,7 +327,7 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep2(Fwd2Params p) {
           for (int k = 0; k < 8; ++k) offA[k] = rA * kSegRow + 16 * ((2 * k + (lo >> 5)) ^ gA);
         }
         const u32x4 drs = tile_rsrc(jn);
-        const uint32_t dlo = sweep_dma_lane_off(opaque_lane(), wave, ROWG);
+        const uint32_t dlo = sweep_dma_lane_off(opaque_lane(), wq, ROWG);
         bf16x8 ring[kPre];
 #pragma unroll
         for (int i = 0; i < kPre; ++i) ring[i] = *(const INFCL_LDS bf16x8*)(cur + offA[i & 7] + kSeg * (i >> 3));
@@ -304,10 +337,10 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep2(Fwd2Params p) {
           mfma_bf16_vgpr(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KS - 1);
           constexpr int SPI = KS / NIW;  // steps per DMA instruction
           if ((s2 + 1) % SPI == 0) {
-            const int kk = (s2 + 1) / SPI - 1;
-            dma16_asm(drs, nxt + 1024 * (wave + 4 * kk), dlo + sweep_dma_kk_off(kk, wave, ROWG));
+            const int kk = kk0 + (s2 + 1) / SPI - 1;
+            dma16_asm(drs, nxt + 1024 * (wq + 4 * kk), dlo + sweep_dma_kk_off(kk, wq, ROWG));
           }
-          if (s2 == (KS > 1 ? 1 : 0)) issue_slot(jn, first_rb, snxt);
+          if (slot_wave && s2 == (KS > 1 ? 1 : 0)) issue_slot(jn, first_rb, snxt);
           if (s2 + kPre < KS) {
             const int n = s2 + kPre;
             ring[s2 % kPre] = *(const INFCL_LDS bf16x8*)(cur + offA[n & 7] + kSeg * (n >> 3));
@@ -315,7 +348,7 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep2(Fwd2Params p) {
           }
         }
       }
-      merge(pr4, ps4);
+      merge(prw, psw);
       // entries off the problem or on the diagonal take no part (uniform test)
       const bool special = (j0 == own0) || (j0 + kSweepBN > b) || !wave_rows_ok;
       // (bitwise operators: no short-circuit branches)
@@ -414,9 +447,9 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep2(Fwd2Params p) {
     }
     {
       const int lpar = (ct_hi - 1 - ct_lo) & 1;  // parity of the last tile
-      const f32x4 r4 = *(const INFCL_LDS f32x4*)&cxR_[lpar][jc][0];
-      const f32x4 s4 = *(const INFCL_LDS f32x4*)&cxS_[lpar][jc][0];
-      merge(r4, s4);
+      float rw[NW], sw[NW];
+      pairs(lpar, rw, sw);
+      merge(rw, sw);
     }
 
     // ---- end of the row block: merge the two lane halves, publish the row pair
@@ -436,7 +469,7 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep2(Fwd2Params p) {
 
 template <int D>
 static int launch_fwd2_d(const Fwd2Params& p, hipStream_t stream) {
-  hipLaunchKernelGGL(fwd_sweep2<D>, dim3(p.Pr * p.Pc), dim3(256), 0, stream, p);
+  hipLaunchKernelGGL(fwd_sweep2<D>, dim3(p.Pr * p.Pc), dim3(64 * kF2NW), 0, stream, p);
   return hipGetLastError() == hipSuccess ? 0 : 1;
 }
 
@@ -446,7 +479,8 @@ bool fwd2_supported(int64_t d, int dtype) { return dtype == 0 && (d == 128 || d 
 void fwd2_grid(int64_t b, int* Pr, int* Pc) {
   const int64_t nRB = (b + kF2BM - 1) / kF2BM, nCT = (b + kSweepBN - 1) / kSweepBN;
   *Pc = (int)(nCT < 8 ? nCT : 8);
-  *Pr = (int)(nRB < 64 ? nRB : 64);
+  const int64_t pmax = 256 / kF2NW;  // P_r P_c <= 2048 / NW: two workgroups per CU with 4 waves, one with 8
+  *Pr = (int)(nRB < pmax ? nRB : pmax);
 }
 
 int launch_fwd2(const void* img, const void* txt, int64_t b, int64_t d, const float* scale, float* rowR, float* rowL,
