@@ -194,7 +194,7 @@ def main():
     alg_fwd_launch = 2.0 * entries * d
     achieved = alg_bwd_launch / (bwd_launch_ms * 1e-3)
     workload = f"symmetric InfoNCE forward+backward, b={b} d={d} {dt_name}, sigma={cfg['sigma']}, s={cfg['scale']}"
-    src = source_hash("bwd.hip", "sweep.hpp", "common.hpp")
+    src = source_hash("bwd.hip", "bwd.hpp", "sweep.hpp", "common.hpp")
     traffic = load_traffic("bwd_sweep", workload, src)
 
     out = {
