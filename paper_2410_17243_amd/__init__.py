@@ -44,6 +44,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is missing: build it with `python -m paper_2410_17243_amd.build`")
+    # torch ships its own HIP runtime under another file name; it must be the
+    # one loaded when this library's kernels register, or the process ends up
+    # with two runtimes and launches on torch's streams fail
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     i64, sz, vp, ip = ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int
     lib.infcl_workspace_size.argtypes = [i64, i64, ip, ctypes.POINTER(sz)]
