@@ -36,6 +36,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=2, help="workload configuration 1..5 (default 2)")
+    ap.add_argument("--dtype", choices=["bf16", "f16", "f32"], default=None,
+                    help="input type instead of the configuration's own (same shapes and scale)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-b", type=int, default=24576,
                     help="batch size of the oracle sample timed on the host (capped at the workload b)")
@@ -110,7 +112,9 @@ def main():
     import paper_2410_17243_amd as infcl
     from paper_2410_17243_amd import synth
 
-    cfg = synth.CONFIGS[a.config]
+    cfg = dict(synth.CONFIGS[a.config])
+    if a.dtype is not None:
+        cfg["dtype"] = a.dtype
     b, d, dt_name = cfg["b"], cfg["d"], cfg["dtype"]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -124,9 +128,10 @@ def main():
 
     note("generating inputs on the host")
     img_np, txt_np = synth.clip_pairs(b, d, cfg["sigma"], seed=0, dtype=dt_name)
-    if dt_name == "bf16":
-        img = torch.from_numpy(img_np.view(np.int16)).view(torch.bfloat16).to(dev)
-        txt = torch.from_numpy(txt_np.view(np.int16)).view(torch.bfloat16).to(dev)
+    if dt_name in ("bf16", "f16"):
+        tdt = torch.bfloat16 if dt_name == "bf16" else torch.float16
+        img = torch.from_numpy(img_np.view(np.int16)).view(tdt).to(dev)
+        txt = torch.from_numpy(txt_np.view(np.int16)).view(tdt).to(dev)
     else:
         img = torch.from_numpy(img_np).to(dev)
         txt = torch.from_numpy(txt_np).to(dev)
@@ -189,7 +194,7 @@ def main():
     value = entries / (ms_per_step * 1e-3)
     bwd_launch_ms = sum(bwd_ms) / len(bwd_ms) / 2.0   # two bwd_sweep launches per infcl_bwd call
     fwd_launch_ms = sum(fwd_ms) / len(fwd_ms)
-    peak = BF16_PEAK if dt_name == "bf16" else FP32_MFMA_PEAK
+    peak = FP32_MFMA_PEAK if dt_name == "f32" else BF16_PEAK  # fp16 and bf16 dense MFMA peaks are equal
     alg_bwd_launch = 3.0 * entries * d      # half of the 6 b^2 d algorithmic backward flops
     alg_fwd_launch = 2.0 * entries * d
     achieved = alg_bwd_launch / (bwd_launch_ms * 1e-3)

@@ -16,7 +16,11 @@
  *
  * Conventions shared by every entry point
  *   - img, txt: device pointers, row-major [b, d], contiguous, 16-byte
- *     aligned; element type given by `dtype` (INFCL_BF16 or INFCL_F32).
+ *     aligned; element type given by `dtype` (INFCL_BF16, INFCL_F32 or
+ *     INFCL_F16).  With 16-bit inputs the products run on the matching
+ *     16-bit MFMA with fp32 accumulation, and the backward rounds its
+ *     gradient weights (the softmax terms) to the input type, round to
+ *     nearest even, before the second product; with f32 everything is fp32.
  *     They are used exactly as given (no normalisation inside the loss).
  *   - scale: device pointer to one float, the logit scale s (1/temperature).
  *   - All float vectors are device pointers, 16-byte aligned.
@@ -29,8 +33,8 @@
  *     launch failure is reported as INFCL_ERR_HIP.  Non-finite input values
  *     are outside the contract (they propagate).
  *   - Supported shapes: 1 <= b <= 2^30; d a multiple of 128 with d <= 1024
- *     for bf16, a multiple of 64 with d <= 512 for f32 (INFCL_ERR_UNSUPPORTED
- *     otherwise).
+ *     for bf16 and f16, a multiple of 64 with d <= 512 for f32
+ *     (INFCL_ERR_UNSUPPORTED otherwise).
  *   - Results are bitwise reproducible for a given (b, d, dtype): no atomics,
  *     all reductions run in a fixed order.
  */
@@ -52,7 +56,9 @@ typedef enum {
   INFCL_ERR_HIP = 4          /* a kernel launch failed                           */
 } infcl_status;
 
-typedef enum { INFCL_BF16 = 0, INFCL_F32 = 1 } infcl_dtype;
+/* Input element types.  INFCL_F16 (IEEE half) is the type of mixed-precision
+ * (AMP) training, under which the paper trains (Sec. 4.1). */
+typedef enum { INFCL_BF16 = 0, INFCL_F32 = 1, INFCL_F16 = 2 } infcl_dtype;
 
 /* Bytes of device workspace that infcl_fwd / infcl_bwd need for (b, d, dtype).
  * The same workspace size serves both calls.  Returns INFCL_ERR_INVALID for a

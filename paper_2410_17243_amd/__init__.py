@@ -26,7 +26,7 @@ LIB_PATH = os.path.join(_PKG, "libinfcl.so")
 HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "infcl.h")
 
 INFCL_OK, INFCL_ERR_INVALID, INFCL_ERR_UNSUPPORTED, INFCL_ERR_WORKSPACE, INFCL_ERR_HIP = range(5)
-INFCL_BF16, INFCL_F32 = 0, 1
+INFCL_BF16, INFCL_F32, INFCL_F16 = 0, 1, 2
 
 _lib = None
 
@@ -87,9 +87,11 @@ def _dtype_code(t) -> int:
 
     if t.dtype == torch.bfloat16:
         return INFCL_BF16
+    if t.dtype == torch.float16:
+        return INFCL_F16
     if t.dtype == torch.float32:
         return INFCL_F32
-    raise TypeError(f"embeddings must be bfloat16 or float32, got {t.dtype}")
+    raise TypeError(f"embeddings must be bfloat16, float16 or float32, got {t.dtype}")
 
 
 def _stream(t):

@@ -13,7 +13,7 @@ int launch_fwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype
 void fwd2_grid(int64_t b, int* Pr, int* Pc);
 int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale,
                const float* lse_r, const float* lse_c, const float* aux, const float* dloss, float* dimg, float* dtxt,
-               float* dscale, float* lse2, double* ds_part, hipStream_t stream);
+               float* dscale, float* lse2, double* ds_part, float* g16, hipStream_t stream);
 bool bwd_supported(int64_t d, int dtype);
 }  // namespace infcl
 
@@ -23,7 +23,7 @@ constexpr int64_t kMaxB = (int64_t)1 << 30;
 
 struct Layout {
   int Pr, Pc;
-  size_t rowR, rowL, colR, colL, udiag, ref2, fwd_part, lse2, bwd_part, total;
+  size_t rowR, rowL, colR, colL, udiag, ref2, fwd_part, lse2, bwd_part, g16, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -51,13 +51,16 @@ Layout make_layout(int64_t b) {
   L.fwd_part = off; off = align256(off + (size_t)((b + 255) / 256) * sizeof(double));
   L.lse2 = off; off = align256(off + 2 * fb);
   L.bwd_part = off; off = align256(off + (size_t)2 * ((b + 63) / 64) * sizeof(double));  // 64 or 128 rows per WG
+  L.g16 = off; off = align256(off + (size_t)(2 + 2 * ((b + 255) / 256)) * sizeof(float));  // fp16 G' scale
   L.total = off;
   return L;
 }
 
 bool aligned(const void* p, size_t a) { return p != nullptr && ((uintptr_t)p % a) == 0; }
 
-bool shape_ok(int64_t b, int64_t d, int dtype) { return b >= 1 && d >= 1 && (dtype == INFCL_BF16 || dtype == INFCL_F32); }
+bool shape_ok(int64_t b, int64_t d, int dtype) {
+  return b >= 1 && d >= 1 && (dtype == INFCL_BF16 || dtype == INFCL_F32 || dtype == INFCL_F16);
+}
 
 bool shape_supported(int64_t b, int64_t d, int dtype) { return b <= kMaxB && infcl::bwd_supported(d, dtype); }
 
@@ -105,7 +108,8 @@ infcl_status infcl_bwd(const void* img, const void* txt, int64_t b, int64_t d, i
   if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)workspace;
   int rc = infcl::launch_bwd(img, txt, b, d, dtype, scale, lse_r, lse_c, aux, dloss, dimg, dtxt, dscale,
-                             (float*)(ws + L.lse2), (double*)(ws + L.bwd_part), (hipStream_t)stream);
+                             (float*)(ws + L.lse2), (double*)(ws + L.bwd_part), (float*)(ws + L.g16),
+                             (hipStream_t)stream);
   if (rc == 2) return INFCL_ERR_UNSUPPORTED;
   return rc == 0 ? INFCL_OK : INFCL_ERR_HIP;
 }

@@ -21,7 +21,7 @@
 //          registers for the whole sweep, swept rows read from LDS with a
 //          row permutation that makes the accumulator usable as GEMM2's operand)
 //   G'     two exp2 per entry (log2 domain), the diagonal from expm1 terms
-//   GEMM2  bf16: the four waves' G' blocks are exchanged through LDS and each
+//   GEMM2  16-bit inputs: the four waves' G' blocks are exchanged through LDS and each
 //          wave multiplies all 128 own rows by its quarter of the features;
 //          fp32: each wave multiplies its own 32 rows by all features.
 // Feature widths whose accumulators do not fit the register file are split in
@@ -42,7 +42,7 @@
 namespace infcl {
 
 constexpr int kBwdBM = 128;  // own rows per workgroup (32 per wave)
-constexpr int kGpBytes = kBwdBM * kBwdBN * 2;  // one bf16 G' exchange buffer
+constexpr int kGpBytes = kBwdBM * kBwdBN * 2;  // one 16-bit G' exchange buffer
 
 // LDS read-ahead (steps) of GEMM1 (build-time tuning knob).
 #ifndef INFCL_BWD_G1_PRE
@@ -52,6 +52,7 @@ constexpr int kGpBytes = kBwdBM * kBwdBN * 2;  // one bf16 G' exchange buffer
 template <typename TIN, int D, int FB, bool PIPE>
 __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   constexpr int ES = sizeof(TIN);
+  constexpr bool F16 = std::is_same<TIN, _Float16>::value;  // fp16 (else bf16) when ES == 2
   constexpr int KS = D / 16;            // 16-wide contraction steps of GEMM1
   constexpr int ROWG = D * ES;          // bytes per row in HBM
   constexpr int TILEB = kBwdBN * ROWG;  // bytes per swept tile
@@ -60,9 +61,9 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   constexpr int NACC = ES == 2 ? 4 * FBW : FB;
   constexpr int NPASS = D / (32 * FB);
   constexpr int GPN = ES == 2 ? (PIPE ? 2 : 1) : 0;  // G' exchange buffers
-  static_assert(!PIPE || ES == 2, "the pipelined schedule is bf16 only");
+  static_assert(!PIPE || ES == 2, "the pipelined schedule is for 16-bit inputs only");
   static_assert(D % (32 * FB) == 0, "pass width must divide d");
-  static_assert(ES == 4 || FB % 4 == 0, "bf16 pass width is a multiple of 128 features");
+  static_assert(ES == 4 || FB % 4 == 0, "16-bit pass width is a multiple of 128 features");
   static_assert(D % 64 == 0 && KS % NIW == 0, "tile DMA layout");
   static_assert((PIPE ? 3 : 2) * TILEB + 3 * 1024 + GPN * kGpBytes + 2048 <= 160 * 1024, "LDS budget");
   __shared__ __attribute__((aligned(1024))) char tA_[TILEB];
@@ -97,7 +98,9 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   const float s = p.scale[0];
   const float k2 = s * kLog2e;
   const float dl = p.dloss ? p.dloss[0] : 1.0f;
-  const float kfin = dl * s / (2.0f * (float)b);
+  // fp16: G' is rounded after scaling by alpha = g16[0], divided out at the end
+  const float g16a = F16 ? p.g16[0] : 1.0f;
+  const float kfin = dl * s / (2.0f * (float)b) * (F16 ? p.g16[1] : 1.0f);
 
   // own operand of GEMM1, held for the whole sweep: row irow, slots 8h..8h+7 of each step
   typedef typename std::conditional<ES == 2, bf16x8, f32x4>::type frag_t;
@@ -201,7 +204,7 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
       __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
 #pragma unroll
       for (int s2 = 0; s2 < KS; ++s2) {
-        mfma_bf16_vgpr(sacc, ring[s2 % kPre], ownf[s2][0], s2 == 0, s2 == KS - 1);
+        mfma16_vgpr<F16>(sacc, ring[s2 % kPre], ownf[s2][0], s2 == 0, s2 == KS - 1);
         dma_step(s2);
         if (s2 + kPre < KS) {
           const int n = s2 + kPre;
@@ -270,12 +273,12 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
     }
     return ds_tile;
   };
-  auto to_bf16 = [](const float (&gv)[16], bf16x8 (&ga)[2]) {
+  auto to_h16 = [&](const float (&gv)[16], bf16x8 (&ga)[2]) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) ga[r >> 3][r & 7] = (__bf16)gv[r];
+    for (int r = 0; r < 16; ++r) ga[r >> 3][r & 7] = to16<F16>(F16 ? gv[r] * g16a : gv[r]);
   };
 
-  // G' exchange buffer (bf16): [128 own rows][32 swept rows], 64-byte rows whose
+  // G' exchange buffer (the input's 16-bit type): [128 own rows][32 swept rows], 64-byte rows whose
   // four 16-byte chunks are XOR-swizzled by (row >> 2) & 3.
   auto put_gp = [&](INFCL_LDS char* gpb, const bf16x8 (&ga)[2]) {
     const int lo = opaque_lane();
@@ -286,7 +289,7 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   };
 
   for (int pass = 0; pass < NPASS; ++pass) {
-    // bf16: dacc[ob * FBW + fbw] holds own block ob (rows 32 ob .. of the
+    // 16-bit: dacc[ob * FBW + fbw] holds own block ob (rows 32 ob .. of the
     // workgroup) x feature block (pass FB + wave FBW + fbw).
     // fp32: dacc[fb] holds this wave's own rows x feature block (pass FB + fb).
     f32x16 dacc[NACC];
@@ -295,7 +298,7 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) dacc[i][r] = 0.f;
 
-    // ---- bf16 GEMM2 of the tile in cur with the G' in gpb, as an explicit
+    // ---- 16-bit GEMM2 of the tile in cur with the G' in gpb, as an explicit
     // software pipeline over its 2 FBW groups (contraction half s2, feature
     // block fbw; 4 MFMAs each, one per own block): stage g issues the LDS reads
     // of group g + 2 and then the MFMAs of group g.  With epi the stages also
@@ -362,7 +365,7 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
               const float x = sacc[r];
               const float pO = exp2_hw(__builtin_fmaf(x, k2, -aO));
               const float pS = exp2_hw(__builtin_fmaf(x, k2, -Lq[(r >> 2) % NL][r & 3]));
-              ga[r >> 3][r & 7] = (__bf16)(pO + pS);
+              ga[r >> 3][r & 7] = to16<F16>(F16 ? (pO + pS) * g16a : pO + pS);
               ds_tile = __builtin_fmaf(pO, x - uO, ds_tile);
             }
           }
@@ -372,7 +375,7 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
         const s16x8 bb = {bq[0][0], bq[0][1], bq[0][2], bq[0][3], bq[1][0], bq[1][1], bq[1][2], bq[1][3]};
 #pragma unroll
         for (int ob = 0; ob < 4; ++ob)
-          dacc[ob * FBW + fbw] = mfma_bf16(A[ob], __builtin_bit_cast(bf16x8, bb), dacc[ob * FBW + fbw]);
+          dacc[ob * FBW + fbw] = mfma16<F16>(A[ob], __builtin_bit_cast(bf16x8, bb), dacc[ob * FBW + fbw]);
         if (g == FBW - 1) readA(1, A);
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -412,7 +415,7 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
         const float d0 = epilogue(0, lA, sacc, gv);
         if (pass == 0) ds_acc += (double)d0;
         bf16x8 ga[2];
-        to_bf16(gv, ga);
+        to_h16(gv, ga);
         put_gp(gp, ga);
       }
       __syncthreads();
@@ -430,7 +433,7 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
         if (tile_special(jt + 1)) {
           float gv[16];
           dn = epilogue(jt + 1, lnxt, sacc, gv);
-          to_bf16(gv, ga);
+          to_h16(gv, ga);
         }
         if (pass == 0 && next) ds_acc += (double)dn;
         put_gp(gp + ((jt + 1) & 1) * kGpBytes, ga);
@@ -458,7 +461,7 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
         if (pass == 0) ds_acc += (double)d0;
         if constexpr (ES == 2) {
           bf16x8 ga[2];
-          to_bf16(gv, ga);
+          to_h16(gv, ga);
           put_gp(gp, ga);
           __syncthreads();
           gemm2_staged(false, cur, gp, lcur, sacc, ga);
@@ -535,10 +538,10 @@ __global__ void __launch_bounds__(256) dscale_finish(const double* part, int64_t
 
 // Pass width: largest FB (32-feature blocks) dividing d/32 whose accumulators
 // (16 FB registers) fit next to the own operand (d/4 or d/2 registers); for
-// bf16 FB is also a multiple of 4 (see the transposing-read addressing).
+// 16-bit inputs FB is also a multiple of 4 (see the transposing-read addressing).
 // Build-time tuning knobs: the register budget shared by the own operand and
 // the gradient accumulators, and whether the three-buffer pipeline is used
-// (bf16 widths whose three tiles fit in LDS).
+// (16-bit widths whose three tiles fit in LDS).
 #ifndef INFCL_BWD_REG_BUDGET
 #define INFCL_BWD_REG_BUDGET 384
 #endif
@@ -553,12 +556,12 @@ static int launch_bwd_d(const BwdParams& p, int nwg, hipStream_t stream) {
   constexpr int NB32 = D / 32;
   constexpr int FBMAX = (INFCL_BWD_REG_BUDGET - OWNREGS) / 16;
   constexpr int FB = [] {
-    int best = ES == 4 ? 1 : 4;  // bf16: at least one 128-feature group
+    int best = ES == 4 ? 1 : 4;  // 16-bit: at least one 128-feature group
     for (int f = 1; f <= NB32; ++f)
       if (NB32 % f == 0 && f <= FBMAX && (ES == 4 || f % 4 == 0)) best = f;
     return best;
   }();
-  static_assert(ES == 4 || FB % 4 == 0, "bf16 pass width must be a multiple of 128 features");
+  static_assert(ES == 4 || FB % 4 == 0, "16-bit pass width must be a multiple of 128 features");
   constexpr int TILEB = kBwdBN * D * ES;
   constexpr bool PIPE = INFCL_BWD_PIPE != 0 && ES == 2 && 3 * (TILEB + 128) + 2 * kGpBytes + 2048 <= 160 * 1024;
   hipLaunchKernelGGL((bwd_sweep<TIN, D, FB, PIPE>), dim3(nwg), dim3(256), 0, stream, p);
@@ -575,9 +578,8 @@ static int launch_bwd_t(const BwdParams& p, int nwg, hipStream_t stream) {
       case 384: return launch_bwd_d<TIN, 384>(p, nwg, stream);
       case 512: return launch_bwd_d<TIN, 512>(p, nwg, stream);
       case 640: return launch_bwd_d<TIN, 640>(p, nwg, stream);
-      case 768: return launch_bwd_d<TIN, 768>(p, nwg, stream);
       case 896: return launch_bwd_d<TIN, 896>(p, nwg, stream);
-      case 1024: return launch_bwd_d<TIN, 1024>(p, nwg, stream);
+      // 768 and 1024 take the single-pass wide-row sweep
     }
   } else {
     switch (d) {
@@ -594,6 +596,65 @@ static int launch_bwd_t(const BwdParams& p, int nwg, hipStream_t stream) {
   return 2;
 }
 
+// fp16 inputs: G' is rounded to fp16 after multiplication by a power of two
+// alpha, and the fp32 accumulators are multiplied by 1/alpha at the end (exact
+// scaling, the role loss scaling plays in mixed-precision training): without
+// it the G' of a well-separated batch (loss near zero) lies below fp16's
+// smallest subnormal, 2^-24, and the gradients would vanish.  alpha maps a
+// bound B on every |G'| to at most 2^14 (fp16's largest finite value is about
+// 2^16): off the diagonal P^r_ij <= 1 - P^r_ii = -expm1(-l^r_i) and
+// P^c_ij <= -expm1(-l^c_j), and |G'_ii| <= -expm1(-l^r_i) - expm1(-l^c_i), so
+// B = max_i(-expm1(-l^r_i)) + max_j(-expm1(-l^c_j)).
+// Per-block maxima (fixed-order tree) of the two terms, then alpha.
+__global__ void __launch_bounds__(256) g16_bound_part(const float* aux, int64_t b, float* part) {
+  __shared__ float sr[256], sc[256];
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  sr[threadIdx.x] = i < b ? -expm1f(-aux[i]) : 0.f;
+  sc[threadIdx.x] = i < b ? -expm1f(-aux[b + i]) : 0.f;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) {
+      sr[threadIdx.x] = fmaxf(sr[threadIdx.x], sr[threadIdx.x + w]);
+      sc[threadIdx.x] = fmaxf(sc[threadIdx.x], sc[threadIdx.x + w]);
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    part[2 * blockIdx.x] = sr[0];
+    part[2 * blockIdx.x + 1] = sc[0];
+  }
+}
+__global__ void __launch_bounds__(256) g16_scale_finish(const float* part, int64_t nblk, float* g16) {
+  __shared__ float sr[256], sc[256];
+  float mr = 0.f, mc = 0.f;
+  for (int64_t k = threadIdx.x; k < nblk; k += 256) {
+    mr = fmaxf(mr, part[2 * k]);
+    mc = fmaxf(mc, part[2 * k + 1]);
+  }
+  sr[threadIdx.x] = mr;
+  sc[threadIdx.x] = mc;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) {
+      sr[threadIdx.x] = fmaxf(sr[threadIdx.x], sr[threadIdx.x + w]);
+      sc[threadIdx.x] = fmaxf(sc[threadIdx.x], sc[threadIdx.x + w]);
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const float B = sr[0] + sc[0];
+    int k = 0;
+    if (B > 0.f) {
+      int e;
+      (void)frexpf(B, &e);  // B = m 2^e, m in [0.5, 1): alpha B = m 2^14 < 2^14
+      k = 14 - e;
+      k = k > 100 ? 100 : k;
+    }
+    g16[0] = ldexpf(1.f, k);
+    g16[1] = ldexpf(1.f, -k);
+  }
+}
+
 // Log-sum-exp vectors rescaled to base 2 (the swept side is streamed through
 // LDS next to every tile and used as is).
 __global__ void __launch_bounds__(256) lse_to_log2(const float* lse_r, const float* lse_c, float* l2r, float* l2c,
@@ -607,24 +668,33 @@ __global__ void __launch_bounds__(256) lse_to_log2(const float* lse_r, const flo
 
 bool bwd_wide_supported(int64_t d, int dtype);
 int bwd_wide_workgroups(int64_t b);
-int launch_bwd_wide(const BwdParams& p, int nwg, hipStream_t stream);
+int launch_bwd_wide(const BwdParams& p, int nwg, bool f16, hipStream_t stream);
 
-// Backward: bf16 with d = 768 or 1024 takes the single-pass wide-row sweep
+// Backward: 16-bit inputs with d = 768 or 1024 take the single-pass wide-row sweep
 // (64 own rows per workgroup), everything else the 128-row sweep above.
 int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale,
                const float* lse_r, const float* lse_c, const float* aux, const float* dloss, float* dimg, float* dtxt,
-               float* dscale, float* lse2, double* ds_part, hipStream_t stream) {
+               float* dscale, float* lse2, double* ds_part, float* g16, hipStream_t stream) {
   const bool wide = bwd_wide_supported(d, dtype);
   const int nwg = wide ? bwd_wide_workgroups(b) : (int)((b + kBwdBM - 1) / kBwdBM);
   auto launch = [&](const BwdParams& q) {
-    if (wide) return launch_bwd_wide(q, nwg, stream);
-    return dtype == 0 ? launch_bwd_t<__bf16>(q, nwg, stream) : launch_bwd_t<float>(q, nwg, stream);
+    if (wide) return launch_bwd_wide(q, nwg, dtype == 2, stream);
+    if (dtype == 0) return launch_bwd_t<__bf16>(q, nwg, stream);
+    if (dtype == 2) return launch_bwd_t<_Float16>(q, nwg, stream);
+    return launch_bwd_t<float>(q, nwg, stream);
   };
   float* l2r = lse2;
   float* l2c = lse2 + b;
-  hipLaunchKernelGGL(lse_to_log2, dim3((unsigned)((b + 255) / 256)), dim3(256), 0, stream, lse_r, lse_c, l2r, l2c, b);
+  const unsigned nblk = (unsigned)((b + 255) / 256);
+  hipLaunchKernelGGL(lse_to_log2, dim3(nblk), dim3(256), 0, stream, lse_r, lse_c, l2r, l2c, b);
   if (hipGetLastError() != hipSuccess) return 1;
+  if (dtype == 2) {  // g16 = (alpha, 1/alpha) followed by 2 nblk block maxima
+    hipLaunchKernelGGL(g16_bound_part, dim3(nblk), dim3(256), 0, stream, aux, b, g16 + 2);
+    hipLaunchKernelGGL(g16_scale_finish, dim3(1), dim3(256), 0, stream, (const float*)(g16 + 2), (int64_t)nblk, g16);
+    if (hipGetLastError() != hipSuccess) return 1;
+  }
   BwdParams p;
+  p.g16 = g16;
   p.b = b;
   p.d = d;
   p.scale = scale;
@@ -658,7 +728,7 @@ int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype
 }
 
 bool bwd_supported(int64_t d, int dtype) {
-  if (dtype == 0) return d % 128 == 0 && d >= 128 && d <= 1024;
+  if (dtype == 0 || dtype == 2) return d % 128 == 0 && d >= 128 && d <= 1024;
   return d % 64 == 0 && d >= 64 && d <= 512;
 }
 

@@ -18,6 +18,7 @@ struct BwdParams {
   const float* dloss;       // device scalar or nullptr (= 1)
   float* dOwn;              // [b, d]
   double* ds_part;          // [gridDim.x]
+  const float* g16;         // fp16 inputs: (alpha, 1/alpha), the power of two G' is scaled by
 };
 
 constexpr int kBwdBN = kSweepBN;  // swept rows per tile

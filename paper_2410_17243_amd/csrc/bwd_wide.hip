@@ -1,5 +1,5 @@
-// Backward sweep for wide rows (bf16, d = 768 or 1024) in a single pass
-// (gfx950).
+// Backward sweep for wide rows (16-bit inputs: bf16 or fp16, d = 768 or
+// 1024) in a single pass (gfx950).
 //
 // Same quantities as the 128-row sweep (Sec. 3.1, Eq. 6-8 completed for both
 // halves of the loss and the scale; the appendix's in-GPU backward recomputes
@@ -15,8 +15,8 @@
 //   join    each wave hands the partner the 8 accumulator entries the
 //           partner finishes (LDS), then adds the partner's half of its own 8;
 //   G'      two exp2 per entry for the wave's 8 entries, the diagonal from
-//           expm1 terms, the dscale contribution; bf16 into the shared G'
-//           block (64 own x 32 swept);
+//           expm1 terms, the dscale contribution; rounded to the input
+//           type into the shared G' block (64 own x 32 swept);
 //   GEMM2   each wave multiplies all 64 own rows' G' by its quarter of the
 //           features of the tile (transposing LDS reads), accumulating in
 //           AGPRs.
@@ -27,7 +27,7 @@ namespace infcl {
 
 constexpr int kWideBM = 64;  // own rows per workgroup
 
-template <int D>
+template <int D, bool F16>
 __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
   constexpr int KS = D / 16;  // 16-wide contraction steps of the full width
   constexpr int KH = KS / 2;  // steps of one wave (half the features)
@@ -44,7 +44,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
   __shared__ __attribute__((aligned(1024))) float lA_[256];
   __shared__ __attribute__((aligned(1024))) float lB_[256];
   // G' of the workgroup's 64 own rows for one tile: 64-byte rows (32 swept
-  // rows, bf16) whose four 16-byte chunks are XOR-swizzled by (row >> 2) & 3
+  // rows, input type) whose four 16-byte chunks are XOR-swizzled by (row >> 2) & 3
   __shared__ __attribute__((aligned(1024))) char gp_[kWideBM * kBwdBN * 2];
   // join: per wave and lane the 8 partial entries its partner finishes
   __shared__ __attribute__((aligned(16))) float xs_[4][64][8];
@@ -71,7 +71,9 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
   const float s = p.scale[0];
   const float k2 = s * kLog2e;
   const float dl = p.dloss ? p.dloss[0] : 1.0f;
-  const float kfin = dl * s / (2.0f * (float)b);
+  // fp16: G' is rounded after scaling by alpha = g16[0], divided out at the end
+  const float g16a = F16 ? p.g16[0] : 1.0f;
+  const float kfin = dl * s / (2.0f * (float)b) * (F16 ? p.g16[1] : 1.0f);
 
   // own operand of GEMM1: row irow, features kh d/2 + 16 s2 + 8h .. +8
   bf16x8 ownf[KH];
@@ -128,7 +130,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
     __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
 #pragma unroll
     for (int s2 = 0; s2 < KH; ++s2) {
-      mfma_bf16_vgpr(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KH - 1);
+      mfma16_vgpr<F16>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KH - 1);
       if ((s2 + 1) % SPI == 0) {
         const int kk = (s2 + 1) / SPI - 1;
         dma16_asm(drs, ddst + 1024 * (wave + 4 * kk), dlo + sweep_dma_kk_off(kk, wave, ROWG));
@@ -180,7 +182,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
         dsv = (ok & !dg) ? dsv : 0.f;
       }
       ds_tile += dsv;
-      ga[i] = (__bf16)gg;
+      ga[i] = to16<F16>(F16 ? gg * g16a : gg);
     }
     const int row = 32 * ob + l32;
     *(INFCL_LDS bf16x8*)(gp + row * 64 + 16 * ((2 * kh + h) ^ ((row >> 2) & 3))) = ga;
@@ -226,7 +228,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
       const s16x8 bb = {q[0][0], q[0][1], q[0][2], q[0][3], q[1][0], q[1][1], q[1][2], q[1][3]};
 #pragma unroll
       for (int o2 = 0; o2 < 2; ++o2)
-        dacc[o2 * FBW + fbw] = mfma_bf16(A[o2], __builtin_bit_cast(bf16x8, bb), dacc[o2 * FBW + fbw]);
+        dacc[o2 * FBW + fbw] = mfma16<F16>(A[o2], __builtin_bit_cast(bf16x8, bb), dacc[o2 * FBW + fbw]);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -283,14 +285,24 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
   if (threadIdx.x == 0) p.ds_part[blockIdx.x] = red[0];
 }
 
-bool bwd_wide_supported(int64_t d, int dtype) { return dtype == 0 && (d == 768 || d == 1024); }
+bool bwd_wide_supported(int64_t d, int dtype) { return (dtype == 0 || dtype == 2) && (d == 768 || d == 1024); }
 
 int bwd_wide_workgroups(int64_t b) { return (int)((b + kWideBM - 1) / kWideBM); }
 
-int launch_bwd_wide(const BwdParams& p, int nwg, hipStream_t stream) {
+int launch_bwd_wide(const BwdParams& p, int nwg, bool f16, hipStream_t stream) {
   switch (p.d) {
-    case 768: hipLaunchKernelGGL(bwd_wide<768>, dim3(nwg), dim3(256), 0, stream, p); break;
-    case 1024: hipLaunchKernelGGL(bwd_wide<1024>, dim3(nwg), dim3(256), 0, stream, p); break;
+    case 768:
+      if (f16)
+        hipLaunchKernelGGL((bwd_wide<768, true>), dim3(nwg), dim3(256), 0, stream, p);
+      else
+        hipLaunchKernelGGL((bwd_wide<768, false>), dim3(nwg), dim3(256), 0, stream, p);
+      break;
+    case 1024:
+      if (f16)
+        hipLaunchKernelGGL((bwd_wide<1024, true>), dim3(nwg), dim3(256), 0, stream, p);
+      else
+        hipLaunchKernelGGL((bwd_wide<1024, false>), dim3(nwg), dim3(256), 0, stream, p);
+      break;
     default: return 2;
   }
   return hipGetLastError() == hipSuccess ? 0 : 1;

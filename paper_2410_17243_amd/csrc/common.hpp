@@ -1,8 +1,9 @@
 // Shared device helpers for the tiled contrastive-loss kernels (gfx950 only).
 //
 // Conventions used by both sweeps
-//   - Matrix products run on the 32x32x16 bf16 MFMA (fp32 accumulate) or the
-//     32x32x2 fp32 MFMA.  For a 32x32 output block, lane L holds column
+//   - Matrix products run on the 32x32x16 bf16 or fp16 MFMA (fp32 accumulate)
+//     or the 32x32x2 fp32 MFMA.  Fragments of both 16-bit types are carried
+//     in bf16x8 registers; only the MFMA opcode and the conversions differ.  For a 32x32 output block, lane L holds column
 //     n = L % 32 and rows m = 8*(r/4) + 4*(L/32) + r%4 for accumulator r = 0..15.
 //     Operand fragments: lane L holds row L % 32 and the 8 consecutive
 //     contraction slots 8*(L/32) .. 8*(L/32)+7 of a 16-wide contraction step.
@@ -19,6 +20,7 @@
 namespace infcl {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -39,6 +41,31 @@ __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2
 
 __device__ __forceinline__ f32x16 mfma_bf16(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+// 16-bit MFMA on fragments held as bf16x8: bf16 operands, or fp16 (F16).
+template <bool F16>
+__device__ __forceinline__ f32x16 mfma16(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  if constexpr (F16)
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                  0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+// float -> 16-bit element, round to nearest even (bf16, or the bits of fp16)
+template <bool F16>
+__device__ __forceinline__ __bf16 to16(float x) {
+  if constexpr (F16)
+    return __builtin_bit_cast(__bf16, (_Float16)x);
+  else
+    return (__bf16)x;
+}
+// 16-bit element (bf16, or fp16 bits) -> float, exact
+template <bool F16>
+__device__ __forceinline__ float from16(__bf16 x) {
+  if constexpr (F16)
+    return (float)__builtin_bit_cast(_Float16, x);
+  else
+    return (float)x;
 }
 __device__ __forceinline__ f32x16 mfma_f32(float a, float b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);

@@ -27,6 +27,8 @@
 // not finite, e.g. while R is still -inf) is redone with the exact max-rescaled
 // merge.  The paper's merge starts from 0; the identity of the merge is the
 // empty sum (R = -inf, l = 0), which is what is used here.
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace infcl {
@@ -110,7 +112,8 @@ __device__ __forceinline__ void fwd_stage_mfma(const INFCL_LDS char* buf, f32x16
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = mfma_bf16(a[mb], bb[nb], acc[mb][nb]);
+        for (int nb = 0; nb < 2; ++nb)
+          acc[mb][nb] = mfma16<std::is_same<TIN, _Float16>::value>(a[mb], bb[nb], acc[mb][nb]);
     }
   } else {
     // fp32: a 16-wide contraction step is 64 bytes; lane half h holds floats 8h..8h+7
@@ -524,8 +527,8 @@ __global__ void __launch_bounds__(256) sum_partials(const double* part, int64_t 
 // ------------------------------------------------------------ host launchers
 bool fwd2_supported(int64_t d, int dtype);
 void fwd2_grid(int64_t b, int* Pr, int* Pc);
-int launch_fwd2(const void* img, const void* txt, int64_t b, int64_t d, const float* scale, float* rowR, float* rowL,
-                float* colR, float* colL, float* udiag, float* ref2, hipStream_t stream);
+int launch_fwd2(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale, float* rowR,
+                float* rowL, float* colR, float* colL, float* udiag, float* ref2, hipStream_t stream);
 
 static int launch_fwd1(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale,
                        hipStream_t stream, int Pr, int Pc, float* rowR, float* rowL, float* colR, float* colL,
@@ -548,6 +551,8 @@ static int launch_fwd1(const void* img, const void* txt, int64_t b, int64_t d, i
   dim3 grid(Pr * Pc);
   if (dtype == 0)
     hipLaunchKernelGGL(fwd_sweep<__bf16>, grid, dim3(256), 0, stream, p);
+  else if (dtype == 2)
+    hipLaunchKernelGGL(fwd_sweep<_Float16>, grid, dim3(256), 0, stream, p);
   else
     hipLaunchKernelGGL(fwd_sweep<float>, grid, dim3(256), 0, stream, p);
   return hipGetLastError() == hipSuccess ? 0 : 1;
@@ -589,7 +594,7 @@ int launch_fwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype
   if (fwd2_supported(d, dtype)) {
     int Pr2 = 0, Pc2 = 0;
     fwd2_grid(b, &Pr2, &Pc2);
-    const int rc = launch_fwd2(img, txt, b, d, scale, rowR, rowL, colR, colL, udiag, ref2, stream);
+    const int rc = launch_fwd2(img, txt, b, d, dtype, scale, rowR, rowL, colR, colL, udiag, ref2, stream);
     if (rc != 0) return rc;
     nrowpart = Pc2;
     ncolpart = Pr2;

@@ -1,17 +1,17 @@
 // Forward sweep of the tiled symmetric InfoNCE loss with resident own rows
-// (bf16 inputs, d <= 512, gfx950).
+// (16-bit inputs: bf16 or fp16, d <= 512, gfx950).
 //
 // What is computed (Sec. 3.1, Eq. 2-5; the in-GPU forward of Sec. 3.2,
 // Alg. 2): the off-diagonal log-sum-exp of every row i and every column j of
 // S = s * img * txt^T, without storing S.
 //
 // Work decomposition.  Workgroup (q, g) of a P_r x P_c grid owns row blocks
-// q, q + P_r, ... of 128 image rows (32 per wave, held in registers as the
-// MFMA operand for the whole block, as Alg. 2 keeps its row tile on chip) and
-// sweeps the text tiles of column group g (32 rows each, streamed through LDS
-// by DMA in the swept-tile layout).  Each tile is one 32 x 32 block of S^T per
-// wave.  Only text tiles move: 32 KiB of DMA per tile and workgroup for
-// 4.2 MFLOP at d = 512.  g = blockIdx mod P_c, so with P_c = 8 the workgroups
+// q, q + P_r, ... of 32 NW image rows (NW = 8 waves by default; 32 rows per
+// wave, held in registers as the MFMA operand for the whole block, as Alg. 2
+// keeps its row tile on chip) and sweeps the text tiles of column group g (32
+// rows each, streamed through LDS by DMA in the swept-tile layout).  Each tile
+// is one 32 x 32 block of S^T per wave.  Only text tiles move: 32 KiB of DMA
+// per tile and workgroup for 8.4 MFLOP at d = 512 with 8 waves.  g = blockIdx mod P_c, so with P_c = 8 the workgroups
 // of a column group share one XCD and its L2.
 //
 // Statistics.  Log-sum-exp values are kept in base 2 as running pairs (R, l)
@@ -41,7 +41,7 @@
 namespace infcl {
 
 struct Fwd2Params {
-  const __bf16* img;  // own rows i, [b, d]
+  const __bf16* img;  // own rows i, [b, d] (bf16, or fp16 bits)
   const __bf16* txt;  // swept rows j, [b, d]
   int64_t b;
   const float* scale;
@@ -69,6 +69,7 @@ constexpr float kTinyBound = 5.421010862427522e-20f;  // 2^-64
 constexpr float kWide = 30.f;
 
 // <img_i, txt_i> in fp32 and its base-2 scaled value; 8 lanes per row.
+template <bool F16>
 __global__ void __launch_bounds__(256) fwd2_diag(const __bf16* img, const __bf16* txt, int64_t b, int64_t d,
                                                  const float* scale, float* udiag, float* ref2) {
   const int64_t i = (int64_t)blockIdx.x * 32 + (threadIdx.x >> 3);
@@ -80,7 +81,7 @@ __global__ void __launch_bounds__(256) fwd2_diag(const __bf16* img, const __bf16
     for (int64_t c = l8; c < d / 8; c += 8) {
       const bf16x8 x = a[c], y = t[c];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc = __builtin_fmaf((float)x[e], (float)y[e], acc);
+      for (int e = 0; e < 8; ++e) acc = __builtin_fmaf(from16<F16>(x[e]), from16<F16>(y[e]), acc);
     }
   }
   acc += shfl_xor(acc, 1);
@@ -140,7 +141,7 @@ __device__ __forceinline__ float pair_level(float R, float l) {
   return l > 0.f ? R + __builtin_amdgcn_logf(l) : -__builtin_inff();
 }
 
-template <int D>
+template <int D, bool F16>
 __global__ void __launch_bounds__(64 * kF2NW, 2) fwd_sweep2(Fwd2Params p) {
   constexpr int NW = kF2NW;
   constexpr int KS = D / 16;
@@ -334,7 +335,7 @@ __global__ void __launch_bounds__(64 * kF2NW, 2) fwd_sweep2(Fwd2Params p) {
         __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
 #pragma unroll
         for (int s2 = 0; s2 < KS; ++s2) {
-          mfma_bf16_vgpr(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KS - 1);
+          mfma16_vgpr<F16>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KS - 1);
           constexpr int SPI = KS / NIW;  // steps per DMA instruction
           if ((s2 + 1) % SPI == 0) {
             const int kk = kk0 + (s2 + 1) / SPI - 1;
@@ -468,12 +469,18 @@ __global__ void __launch_bounds__(64 * kF2NW, 2) fwd_sweep2(Fwd2Params p) {
 }
 
 template <int D>
-static int launch_fwd2_d(const Fwd2Params& p, hipStream_t stream) {
-  hipLaunchKernelGGL(fwd_sweep2<D>, dim3(p.Pr * p.Pc), dim3(64 * kF2NW), 0, stream, p);
+static int launch_fwd2_d(const Fwd2Params& p, bool f16, hipStream_t stream) {
+  if (f16)
+    hipLaunchKernelGGL((fwd_sweep2<D, true>), dim3(p.Pr * p.Pc), dim3(64 * kF2NW), 0, stream, p);
+  else
+    hipLaunchKernelGGL((fwd_sweep2<D, false>), dim3(p.Pr * p.Pc), dim3(64 * kF2NW), 0, stream, p);
   return hipGetLastError() == hipSuccess ? 0 : 1;
 }
 
-bool fwd2_supported(int64_t d, int dtype) { return dtype == 0 && (d == 128 || d == 256 || d == 384 || d == 512); }
+// 16-bit inputs (bf16 = 0, fp16 = 2) with d <= 512
+bool fwd2_supported(int64_t d, int dtype) {
+  return (dtype == 0 || dtype == 2) && (d == 128 || d == 256 || d == 384 || d == 512);
+}
 
 // Grid of the resident-rows forward for b samples.
 void fwd2_grid(int64_t b, int* Pr, int* Pc) {
@@ -483,10 +490,15 @@ void fwd2_grid(int64_t b, int* Pr, int* Pc) {
   *Pr = (int)(nRB < pmax ? nRB : pmax);
 }
 
-int launch_fwd2(const void* img, const void* txt, int64_t b, int64_t d, const float* scale, float* rowR, float* rowL,
-                float* colR, float* colL, float* udiag, float* ref2, hipStream_t stream) {
-  hipLaunchKernelGGL(fwd2_diag, dim3((unsigned)((b + 31) / 32)), dim3(256), 0, stream, (const __bf16*)img,
-                     (const __bf16*)txt, b, d, scale, udiag, ref2);
+int launch_fwd2(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale, float* rowR,
+                float* rowL, float* colR, float* colL, float* udiag, float* ref2, hipStream_t stream) {
+  const bool f16 = dtype == 2;
+  if (f16)
+    hipLaunchKernelGGL(fwd2_diag<true>, dim3((unsigned)((b + 31) / 32)), dim3(256), 0, stream, (const __bf16*)img,
+                       (const __bf16*)txt, b, d, scale, udiag, ref2);
+  else
+    hipLaunchKernelGGL(fwd2_diag<false>, dim3((unsigned)((b + 31) / 32)), dim3(256), 0, stream, (const __bf16*)img,
+                       (const __bf16*)txt, b, d, scale, udiag, ref2);
   if (hipGetLastError() != hipSuccess) return 1;
   Fwd2Params p;
   p.img = (const __bf16*)img;
@@ -502,10 +514,10 @@ int launch_fwd2(const void* img, const void* txt, int64_t b, int64_t d, const fl
   p.nRB = (int)((b + kF2BM - 1) / kF2BM);
   p.nCT = (int)((b + kSweepBN - 1) / kSweepBN);
   switch (d) {
-    case 128: return launch_fwd2_d<128>(p, stream);
-    case 256: return launch_fwd2_d<256>(p, stream);
-    case 384: return launch_fwd2_d<384>(p, stream);
-    case 512: return launch_fwd2_d<512>(p, stream);
+    case 128: return launch_fwd2_d<128>(p, f16, stream);
+    case 256: return launch_fwd2_d<256>(p, f16, stream);
+    case 384: return launch_fwd2_d<384>(p, f16, stream);
+    case 512: return launch_fwd2_d<512>(p, f16, stream);
   }
   return 2;
 }

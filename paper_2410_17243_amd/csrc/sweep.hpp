@@ -41,27 +41,33 @@ __device__ __forceinline__ uint32_t sweep_dma_kk_off(int kk, int wave, int rowg)
   return (uint32_t)(4 * (k & 7) * rowg + 256 * (k >> 3));
 }
 
-// bf16 32x32x16 MFMA accumulating in VGPRs (the compiler would place an
-// accumulation chain in AGPRs, which the backward needs for its gradients).
-// Volatile, so that the chain keeps its order with interleaved DMA
-// instructions.  Hazards inside inline assembly are not checked by the
-// compiler: two wait states precede each MFMA (a VALU write of a source
-// operand, e.g. an operand the compiler restores with v_accvgpr_read, must be
-// two wait states old), and the last MFMA of a chain is followed by the wait
-// states a VALU read of its result needs, inside the same statement so that
-// nothing reads the accumulator earlier.
-__device__ __forceinline__ void mfma_bf16_vgpr(f32x16& acc, const bf16x8& a, const bf16x8& b, bool first,
-                                               bool last) {
-  if (first && last)
-    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, 0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3"
-                 : "=&v"(acc) : "v"(a), "v"(b));
-  else if (first)
-    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "v"(b));
-  else if (last)
-    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3"
-                 : "+v"(acc) : "v"(a), "v"(b));
-  else
-    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "v"(b));
+// 16-bit 32x32x16 MFMA (bf16, or fp16 with F16) accumulating in VGPRs (the
+// compiler would place an accumulation chain in AGPRs, which the backward
+// needs for its gradients).  Volatile, so that the chain keeps its order with
+// interleaved DMA instructions.  Hazards inside inline assembly are not
+// checked by the compiler: two wait states precede each MFMA (a VALU write of
+// a source operand, e.g. an operand the compiler restores with
+// v_accvgpr_read, must be two wait states old), and the last MFMA of a chain
+// is followed by the wait states a VALU read of its result needs, inside the
+// same statement so that nothing reads the accumulator earlier.
+#define INFCL_MFMA16_VGPR(OP)                                                                                  \
+  if (first && last)                                                                                           \
+    asm volatile("s_nop 1\n\t" OP " %0, %1, %2, 0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3" : "=&v"(acc) : "v"(a), "v"(b)); \
+  else if (first)                                                                                              \
+    asm volatile("s_nop 1\n\t" OP " %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "v"(b));                              \
+  else if (last)                                                                                               \
+    asm volatile("s_nop 1\n\t" OP " %0, %1, %2, %0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3" : "+v"(acc) : "v"(a), "v"(b)); \
+  else                                                                                                         \
+    asm volatile("s_nop 1\n\t" OP " %0, %1, %2, %0" : "+v"(acc) : "v"(a), "v"(b));
+
+template <bool F16>
+__device__ __forceinline__ void mfma16_vgpr(f32x16& acc, const bf16x8& a, const bf16x8& b, bool first, bool last) {
+  if constexpr (F16) {
+    INFCL_MFMA16_VGPR("v_mfma_f32_32x32x16_f16")
+  } else {
+    INFCL_MFMA16_VGPR("v_mfma_f32_32x32x16_bf16")
+  }
 }
+#undef INFCL_MFMA16_VGPR
 
 }  // namespace infcl

@@ -13,8 +13,8 @@ available; these synthetic pairs stand in for them):
   txt = L2norm(img + sigma * n)                       mode "weak" (noise added to
                                                       the unit vector itself)
 
-Normalisation is done in float32; the bf16 variant rounds the float32 values to
-bfloat16 with round-to-nearest-even.  The positive cosine is about
+Normalisation is done in float32; the bf16 and f16 variants round the float32
+values to bfloat16 or IEEE half with round-to-nearest-even.  The positive cosine is about
 1/sqrt(1 + sigma^2) in mode "clip" and about 1/sqrt(1 + sigma^2 d) in "weak".
 """
 
@@ -45,13 +45,14 @@ def _l2norm_rows(a: np.ndarray) -> np.ndarray:
 def clip_pairs(b: int, d: int, sigma: float, seed: int = 0, dtype: str = "bf16", mode: str = "clip"):
     """Return (img, txt) as numpy arrays of shape [b, d].
 
-    dtype "bf16" returns uint16 bfloat16 bit patterns; "f32" returns float32.
+    dtype "bf16" returns uint16 bfloat16 bit patterns, "f16" uint16 IEEE half
+    bit patterns; "f32" returns float32.
     """
-    if dtype not in ("bf16", "f32"):
-        raise ValueError(f"dtype must be 'bf16' or 'f32', got {dtype!r}")
+    if dtype not in ("bf16", "f16", "f32"):
+        raise ValueError(f"dtype must be 'bf16', 'f16' or 'f32', got {dtype!r}")
     if mode not in ("clip", "weak"):
         raise ValueError(f"mode must be 'clip' or 'weak', got {mode!r}")
-    out_dt = np.uint16 if dtype == "bf16" else np.float32
+    out_dt = np.float32 if dtype == "f32" else np.uint16
     img = np.empty((b, d), dtype=out_dt)
     txt = np.empty((b, d), dtype=out_dt)
     sig = np.float32(sigma)
@@ -68,6 +69,9 @@ def clip_pairs(b: int, d: int, sigma: float, seed: int = 0, dtype: str = "bf16",
         if dtype == "bf16":
             img[r0:r1] = f32_to_bf16_bits(im)
             txt[r0:r1] = f32_to_bf16_bits(tx)
+        elif dtype == "f16":
+            img[r0:r1] = im.astype(np.float16).view(np.uint16)  # round to nearest even
+            txt[r0:r1] = tx.astype(np.float16).view(np.uint16)
         else:
             img[r0:r1] = im
             txt[r0:r1] = tx
@@ -75,9 +79,11 @@ def clip_pairs(b: int, d: int, sigma: float, seed: int = 0, dtype: str = "bf16",
 
 
 def as_f64(a: np.ndarray, dtype: str) -> np.ndarray:
-    """Exact float64 view of generator output (bf16 bits or float32)."""
+    """Exact float64 view of generator output (bf16 or f16 bits, or float32)."""
     if dtype == "bf16":
         return bf16_bits_to_f32(a).astype(np.float64)
+    if dtype == "f16":
+        return np.asarray(a, dtype=np.uint16).view(np.float16).astype(np.float64)
     return np.asarray(a, dtype=np.float32).astype(np.float64)
 
 

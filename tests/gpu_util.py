@@ -11,9 +11,10 @@ from paper_2410_17243_amd import synth
 
 
 def device_inputs(img, txt, dtype):
-    if dtype == "bf16":
-        I = torch.from_numpy(img.view(np.int16)).view(torch.bfloat16).cuda()
-        T = torch.from_numpy(txt.view(np.int16)).view(torch.bfloat16).cuda()
+    if dtype in ("bf16", "f16"):
+        tdt = torch.bfloat16 if dtype == "bf16" else torch.float16
+        I = torch.from_numpy(img.view(np.int16)).view(tdt).cuda()
+        T = torch.from_numpy(txt.view(np.int16)).view(tdt).cuda()
     else:
         I = torch.from_numpy(np.ascontiguousarray(img, dtype=np.float32)).cuda()
         T = torch.from_numpy(np.ascontiguousarray(txt, dtype=np.float32)).cuda()

@@ -46,6 +46,8 @@ def test_workspace_size_is_linear_in_b():
     (16, 512, 7, infcl.INFCL_ERR_INVALID), (16, 100, 0, infcl.INFCL_ERR_UNSUPPORTED),
     (16, 2048, 0, infcl.INFCL_ERR_UNSUPPORTED), (16, 1024, 1, infcl.INFCL_ERR_UNSUPPORTED),
     (16, 64, 0, infcl.INFCL_ERR_UNSUPPORTED), (16, 64, 1, infcl.INFCL_OK), ((1 << 30) + 1, 512, 0, infcl.INFCL_ERR_UNSUPPORTED),
+    (16, 512, 2, infcl.INFCL_OK), (16, 1024, 2, infcl.INFCL_OK), (16, 64, 2, infcl.INFCL_ERR_UNSUPPORTED),
+    (16, 100, 2, infcl.INFCL_ERR_UNSUPPORTED), (16, 512, 3, infcl.INFCL_ERR_INVALID),
 ])
 def test_workspace_size_validation(b, d, dt, expect):
     assert _ws(b, d, dt)[0] == expect

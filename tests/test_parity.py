@@ -4,7 +4,10 @@ Bars (bf16 embeddings, fp32 accumulation): loss relative error <= 1e-3;
 gradients max|diff| / max|ref| <= 2e-2; dscale relative <= 2e-2; the row and
 column log-sum-exp within the fp32-accumulation bound of gpu_util.lse_tol.
 fp32 embeddings: loss <= 1e-5 relative, gradients <= 1e-4 (the G' operand of
-the second product stays fp32 there).
+the second product stays fp32 there).  fp16 embeddings: the same bars as bf16
+for the loss and log-sum-exp; gradients and dscale <= 2.5e-3: G' is rounded to
+fp16 (unit roundoff 2^-11) instead of bf16 (2^-8), and both bars are about
+five unit roundoffs of the G' type (5 * 2^-8 = 1.95e-2, 5 * 2^-11 = 2.4e-3).
 """
 
 import math
@@ -19,8 +22,8 @@ pytestmark = pytest.mark.gpu
 
 
 def _check(gpu, ref, dI, dT, ds, s, d, dtype, loss_tol=None, grad_tol=None):
-    loss_tol = loss_tol or (1e-3 if dtype == "bf16" else 1e-5)
-    grad_tol = grad_tol or (2e-2 if dtype == "bf16" else 1e-4)
+    loss_tol = loss_tol or {"bf16": 1e-3, "f16": 1e-3, "f32": 1e-5}[dtype]
+    grad_tol = grad_tol or {"bf16": 2e-2, "f16": 2.5e-3, "f32": 1e-4}[dtype]
     print(f"loss gpu {gpu['loss64']:.9e} ref {ref['loss']:.9e} | lse_r err {np.max(np.abs(gpu['lse_r'] - ref['lse_r'])):.2e}"
           f" lse_c err {np.max(np.abs(gpu['lse_c'] - ref['lse_c'])):.2e} | dI {max_rel(gpu['dI'], dI):.2e}"
           f" dT {max_rel(gpu['dT'], dT):.2e} | ds gpu {gpu['dscale']:.6e} ref {ds:.6e}", flush=True)
@@ -109,6 +112,21 @@ def test_weak_positive_reading_bf16():
 def test_dloss_scaling_bf16():
     gpu, fwd, dI, dT, ds, s = _case(700, 256, 20.0, dloss=-0.37, seed=5)
     _check(gpu, fwd, dI, dT, ds, s, 256, "bf16")
+
+
+@pytest.mark.parametrize("b,d", [(1, 128), (65, 128), (1025, 256), (777, 512), (777, 640), (700, 768), (600, 1024)])
+def test_fp16_inputs(b, d):
+    """IEEE half embeddings (the paper's mixed-precision training type): the
+    resident-rows forward (d <= 512), the streamed forward (d > 512), the
+    128-row backward and the wide backward (d = 768, 1024)."""
+    gpu, fwd, dI, dT, ds, s = _case(b, d, 14.29, dtype="f16", seed=b + d)
+    _check(gpu, fwd, dI, dT, ds, s, d, "f16")
+
+
+@pytest.mark.parametrize("s,sigma", [(50.0, 1.0), (100.0, 0.5)])
+def test_fp16_scales(s, sigma):
+    gpu, fwd, dI, dT, ds, s32 = _case(1536, 512, s, sigma=sigma, dtype="f16", seed=11)
+    _check(gpu, fwd, dI, dT, ds, s32, 512, "f16")
 
 
 @pytest.mark.parametrize("b,d", [(1, 64), (17, 64), (300, 192), (1024, 512)])
