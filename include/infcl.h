@@ -96,6 +96,59 @@ infcl_status infcl_bwd(const void* img, const void* txt, int64_t b, int64_t d, i
                        const float* dloss, float* dimg, float* dtxt, float* dscale,
                        void* workspace, size_t ws_bytes, void* stream);
 
+/* ---- One GPU's share of a batch sharded over n GPUs (Sec. 3.2, cross-GPU
+ * tiling, Alg. 1 and Alg. 3).  GPU g owns samples [r0, r0 + bs): its rows of
+ * S (image side) and its columns (text side).  Instead of the paper's ring,
+ * which moves text blocks between GPUs step by step, every GPU holds all of
+ * img and txt (an all-gather of 2 b d elements per GPU), computes its rows
+ * against all b columns, and one exchange of column pairs completes the
+ * column statistics:
+ *   1. infcl_fwd_shard on every GPU: row statistics of own rows (kept in the
+ *      workspace) and one pair per column over own rows, for all b columns;
+ *   2. all-to-all: GPU g receives, from each of the n GPUs, the pairs of its
+ *      own columns [r0, r0 + bs);
+ *   3. infcl_fwd_shard_finish on every GPU: own lse_r, lse_c, aux and its
+ *      share of the loss (loss = sum of the shares: an all-reduce);
+ *   4. all-gather of lse_r, lse_c and aux (4 b bytes each);
+ *   5. infcl_bwd_shard on every GPU: dimg and dtxt of own samples, and its
+ *      share of dscale (dscale = sum of the shares).
+ * The kernels are those of infcl_fwd / infcl_bwd on a rectangle of bs own
+ * rows by b columns.  r0 must be a multiple of 32 and 1 <= bs <= b - r0
+ * (INFCL_ERR_INVALID otherwise).  The workspace is that of
+ * infcl_workspace_size(b, d, dtype); infcl_fwd_shard_finish must get the same
+ * workspace as the infcl_fwd_shard call of its shard, untouched in between.
+ * With one shard (r0 = 0, bs = b) the three calls compute what infcl_fwd
+ * and infcl_bwd compute. */
+
+/* Step 1.  colpair [2b] float (device, 16-byte aligned): colpair[j] = R_j and
+ * colpair[b + j] = l_j, the base-2 log-sum-exp pair (log2 l_j + R_j) of
+ * column j over own rows i != j.  The forward's ordinary outputs are not
+ * produced here. */
+infcl_status infcl_fwd_shard(const void* img, const void* txt, int64_t b, int64_t d, int dtype,
+                             int64_t r0, int64_t bs, const float* scale, float* colpair,
+                             void* workspace, size_t ws_bytes, void* stream);
+
+/* Step 3.  colpairs [nparts][2 bs] float (device): for each of the nparts
+ * shards, the R values then the l values of this shard's columns
+ * [r0, r0 + bs) from that shard's colpair.  Outputs for own samples
+ * (device): lse_r [bs], lse_c [bs], aux [3 bs] (laid out as infcl_fwd's aux
+ * with bs in place of b) and loss_part [1] double, this shard's share
+ * (sum over own samples of (r_i - x_ii) + (c_i - x_ii)) / (2b). */
+infcl_status infcl_fwd_shard_finish(int64_t b, int64_t d, int dtype, int64_t r0, int64_t bs,
+                                    int64_t nparts, const float* colpairs, const float* scale,
+                                    float* lse_r, float* lse_c, float* aux, double* loss_part,
+                                    void* workspace, size_t ws_bytes, void* stream);
+
+/* Step 5.  lse_r, lse_c [b] and aux [3b] cover all b samples (the all-gather
+ * of every shard's finish outputs, in sample order).  Outputs (device):
+ * dimg, dtxt [bs, d] float, the gradients of own samples, and
+ * dscale_part [1] double, this shard's share of dloss * dL/ds. */
+infcl_status infcl_bwd_shard(const void* img, const void* txt, int64_t b, int64_t d, int dtype,
+                             int64_t r0, int64_t bs, const float* scale, const float* lse_r,
+                             const float* lse_c, const float* aux, const float* dloss,
+                             float* dimg, float* dtxt, double* dscale_part,
+                             void* workspace, size_t ws_bytes, void* stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* infcl_status_str(int status);
 

@@ -56,6 +56,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.infcl_fwd.restype = ip
     lib.infcl_bwd.argtypes = [vp, vp, i64, i64, ip, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.infcl_bwd.restype = ip
+    lib.infcl_fwd_shard.argtypes = [vp, vp, i64, i64, ip, i64, i64, vp, vp, vp, sz, vp]
+    lib.infcl_fwd_shard.restype = ip
+    lib.infcl_fwd_shard_finish.argtypes = [i64, i64, ip, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.infcl_fwd_shard_finish.restype = ip
+    lib.infcl_bwd_shard.argtypes = [vp, vp, i64, i64, ip, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.infcl_bwd_shard.restype = ip
     lib.infcl_status_str.argtypes = [ip]
     lib.infcl_status_str.restype = ctypes.c_char_p
     _lib = lib
@@ -121,6 +127,31 @@ def infcl_bwd(img, txt, scale, lse_r, lse_c, aux, dloss, dimg, dtxt, dscale, wor
                                      _ptr(lse_c), _ptr(aux), _ptr(dloss), _ptr(dimg), _ptr(dtxt), _ptr(dscale),
                                      _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(img)),
            "infcl_bwd")
+
+
+def infcl_fwd_shard(img, txt, scale, r0, bs, colpair, workspace):
+    b, d = img.shape
+    _check(load_library().infcl_fwd_shard(_ptr(img), _ptr(txt), b, d, _dtype_code(img), int(r0), int(bs), _ptr(scale),
+                                           _ptr(colpair), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                           _stream(img)), "infcl_fwd_shard")
+
+
+def infcl_fwd_shard_finish(b, d, dtype, r0, bs, colpairs, scale, lse_r, lse_c, aux, loss_part, workspace):
+    nparts = colpairs.shape[0]
+    _check(load_library().infcl_fwd_shard_finish(int(b), int(d), int(dtype), int(r0), int(bs), int(nparts),
+                                                  _ptr(colpairs), _ptr(scale), _ptr(lse_r), _ptr(lse_c), _ptr(aux),
+                                                  _ptr(loss_part), _ptr(workspace),
+                                                  workspace.numel() * workspace.element_size(), _stream(scale)),
+           "infcl_fwd_shard_finish")
+
+
+def infcl_bwd_shard(img, txt, scale, r0, bs, lse_r, lse_c, aux, dloss, dimg, dtxt, dscale_part, workspace):
+    b, d = img.shape
+    _check(load_library().infcl_bwd_shard(_ptr(img), _ptr(txt), b, d, _dtype_code(img), int(r0), int(bs), _ptr(scale),
+                                           _ptr(lse_r), _ptr(lse_c), _ptr(aux), _ptr(dloss), _ptr(dimg), _ptr(dtxt),
+                                           _ptr(dscale_part), _ptr(workspace),
+                                           workspace.numel() * workspace.element_size(), _stream(img)),
+           "infcl_bwd_shard")
 
 
 # ------------------------------------------------------------- torch wrappers

@@ -8,12 +8,21 @@
 
 namespace infcl {
 int launch_fwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale, float* loss,
-               double* loss64, float* lse_r, float* lse_c, float* aux, char* ws, hipStream_t stream, int Pr, int Pc,
-               float* rowR, float* rowL, float* colR, float* colL, float* udiag, float* ref2, double* partial);
-void fwd2_grid(int64_t b, int* Pr, int* Pc);
-int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale,
-               const float* lse_r, const float* lse_c, const float* aux, const float* dloss, float* dimg, float* dtxt,
-               float* dscale, float* lse2, double* ds_part, float* g16, hipStream_t stream);
+               double* loss64, float* lse_r, float* lse_c, float* aux, hipStream_t stream, float* rowR, float* rowL,
+               float* colR, float* colL, float* udiag, float* ref2, double* partial);
+int launch_fwd_shard(const void* img, const void* txt, int64_t b, int64_t d, int dtype, int64_t r0, int64_t nrows,
+                     const float* scale, float* colpair, hipStream_t stream, float* rowR, float* rowL, float* colR,
+                     float* colL, float* udiag, float* ref2);
+int launch_fwd_shard_finish(int64_t b, int64_t d, int dtype, int64_t r0, int64_t nrows, int64_t nparts,
+                            const float* colpairs, const float* scale, float* lse_r, float* lse_c, float* aux,
+                            double* loss_part, hipStream_t stream, const float* rowR, const float* rowL,
+                            const float* udiag, double* partial);
+void fwd1_grid(int64_t b, int64_t nrows, int* Pr, int* Pc);
+void fwd2_grid(int64_t b, int64_t nrows, int* Pr, int* Pc);
+int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, int64_t r0, int64_t nrows,
+               const float* scale, const float* lse_r, const float* lse_c, const float* aux, const float* dloss,
+               float* dimg, float* dtxt, float* dscale, double* dscale64, float* lse2, double* ds_part, float* g16,
+               hipStream_t stream);
 bool bwd_supported(int64_t d, int dtype);
 }  // namespace infcl
 
@@ -22,24 +31,21 @@ namespace {
 constexpr int64_t kMaxB = (int64_t)1 << 30;
 
 struct Layout {
-  int Pr, Pc;
   size_t rowR, rowL, colR, colL, udiag, ref2, fwd_part, lse2, bwd_part, g16, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Forward grid of the streamed-tiles sweep: Pc column groups (one per XCD
-// when there are enough column tiles) times Pr row groups, about two
-// workgroups per compute unit.  The partial-pair regions also hold those of
-// the resident-rows sweep (Pc2 row partials, Pr2 column partials).
+// Partial-pair regions sized for either forward sweep over all b rows
+// (streamed tiles: 4 Pc row partials, Pr column partials; resident rows: Pc2
+// and Pr2).  A shard of nrows <= b rows needs no more: its grids have at most
+// as many row groups, and its row partials are nrows long.
 Layout make_layout(int64_t b) {
   Layout L;
-  const int64_t nRT = (b + 63) / 64, nCT = (b + 255) / 256;
-  L.Pc = (int)(nCT < 8 ? nCT : 8);
-  L.Pr = (int)(nRT < 64 ? nRT : 64);
-  int Pr2 = 0, Pc2 = 0;
-  infcl::fwd2_grid(b, &Pr2, &Pc2);
-  const size_t nrow = (size_t)(L.Pc * 4 > Pc2 ? L.Pc * 4 : Pc2), ncol = (size_t)(L.Pr > Pr2 ? L.Pr : Pr2);
+  int Pr = 0, Pc = 0, Pr2 = 0, Pc2 = 0;
+  infcl::fwd1_grid(b, b, &Pr, &Pc);
+  infcl::fwd2_grid(b, b, &Pr2, &Pc2);
+  const size_t nrow = (size_t)(Pc * 4 > Pc2 ? Pc * 4 : Pc2), ncol = (size_t)(Pr > Pr2 ? Pr : Pr2);
   size_t off = 0;
   const size_t fb = (size_t)b * sizeof(float);
   L.rowR = off; off = align256(off + nrow * fb);
@@ -64,6 +70,12 @@ bool shape_ok(int64_t b, int64_t d, int dtype) {
 
 bool shape_supported(int64_t b, int64_t d, int dtype) { return b <= kMaxB && infcl::bwd_supported(d, dtype); }
 
+// A shard: own samples [r0, r0 + bs) of the batch, r0 a multiple of 32 (so
+// that own row blocks line up with the 32-row swept tiles).
+bool shard_ok(int64_t b, int64_t r0, int64_t bs) { return r0 >= 0 && r0 % 32 == 0 && bs >= 1 && r0 + bs <= b; }
+
+constexpr int64_t kMaxParts = 1 << 16;  // shards whose column pairs one finish merges
+
 }  // namespace
 
 extern "C" {
@@ -87,8 +99,8 @@ infcl_status infcl_fwd(const void* img, const void* txt, int64_t b, int64_t d, i
   const Layout L = make_layout(b);
   if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)workspace;
-  int rc = infcl::launch_fwd(img, txt, b, d, dtype, scale, loss, loss64, lse_r, lse_c, aux, ws, (hipStream_t)stream,
-                             L.Pr, L.Pc, (float*)(ws + L.rowR), (float*)(ws + L.rowL), (float*)(ws + L.colR),
+  int rc = infcl::launch_fwd(img, txt, b, d, dtype, scale, loss, loss64, lse_r, lse_c, aux, (hipStream_t)stream,
+                             (float*)(ws + L.rowR), (float*)(ws + L.rowL), (float*)(ws + L.colR),
                              (float*)(ws + L.colL), (float*)(ws + L.udiag), (float*)(ws + L.ref2),
                              (double*)(ws + L.fwd_part));
   return rc == 0 ? INFCL_OK : INFCL_ERR_HIP;
@@ -107,8 +119,66 @@ infcl_status infcl_bwd(const void* img, const void* txt, int64_t b, int64_t d, i
   const Layout L = make_layout(b);
   if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)workspace;
-  int rc = infcl::launch_bwd(img, txt, b, d, dtype, scale, lse_r, lse_c, aux, dloss, dimg, dtxt, dscale,
+  int rc = infcl::launch_bwd(img, txt, b, d, dtype, 0, b, scale, lse_r, lse_c, aux, dloss, dimg, dtxt, dscale, nullptr,
                              (float*)(ws + L.lse2), (double*)(ws + L.bwd_part), (float*)(ws + L.g16),
+                             (hipStream_t)stream);
+  if (rc == 2) return INFCL_ERR_UNSUPPORTED;
+  return rc == 0 ? INFCL_OK : INFCL_ERR_HIP;
+}
+
+// ------------------------------------------------------------------ shards
+
+infcl_status infcl_fwd_shard(const void* img, const void* txt, int64_t b, int64_t d, int dtype, int64_t r0,
+                             int64_t bs, const float* scale, float* colpair, void* workspace, size_t ws_bytes,
+                             void* stream) {
+  if (!shape_ok(b, d, dtype) || !shard_ok(b, r0, bs)) return INFCL_ERR_INVALID;
+  if (!aligned(img, 16) || !aligned(txt, 16) || !aligned(scale, 4) || !aligned(colpair, 16) ||
+      !aligned(workspace, 256))
+    return INFCL_ERR_INVALID;
+  if (!shape_supported(b, d, dtype)) return INFCL_ERR_UNSUPPORTED;
+  const Layout L = make_layout(b);
+  if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
+  char* ws = (char*)workspace;
+  int rc = infcl::launch_fwd_shard(img, txt, b, d, dtype, r0, bs, scale, colpair, (hipStream_t)stream,
+                                   (float*)(ws + L.rowR), (float*)(ws + L.rowL), (float*)(ws + L.colR),
+                                   (float*)(ws + L.colL), (float*)(ws + L.udiag), (float*)(ws + L.ref2));
+  return rc == 0 ? INFCL_OK : INFCL_ERR_HIP;
+}
+
+infcl_status infcl_fwd_shard_finish(int64_t b, int64_t d, int dtype, int64_t r0, int64_t bs, int64_t nparts,
+                                    const float* colpairs, const float* scale, float* lse_r, float* lse_c,
+                                    float* aux, double* loss_part, void* workspace, size_t ws_bytes, void* stream) {
+  if (!shape_ok(b, d, dtype) || !shard_ok(b, r0, bs) || nparts < 1 || nparts > kMaxParts) return INFCL_ERR_INVALID;
+  if (!aligned(colpairs, 4) || !aligned(scale, 4) || !aligned(lse_r, 4) || !aligned(lse_c, 4) || !aligned(aux, 4) ||
+      !aligned(loss_part, 8) || !aligned(workspace, 256))
+    return INFCL_ERR_INVALID;
+  if (!shape_supported(b, d, dtype)) return INFCL_ERR_UNSUPPORTED;
+  const Layout L = make_layout(b);
+  if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
+  char* ws = (char*)workspace;
+  int rc = infcl::launch_fwd_shard_finish(b, d, dtype, r0, bs, nparts, colpairs, scale, lse_r, lse_c, aux, loss_part,
+                                          (hipStream_t)stream, (const float*)(ws + L.rowR),
+                                          (const float*)(ws + L.rowL), (const float*)(ws + L.udiag),
+                                          (double*)(ws + L.fwd_part));
+  return rc == 0 ? INFCL_OK : INFCL_ERR_HIP;
+}
+
+infcl_status infcl_bwd_shard(const void* img, const void* txt, int64_t b, int64_t d, int dtype, int64_t r0,
+                             int64_t bs, const float* scale, const float* lse_r, const float* lse_c, const float* aux,
+                             const float* dloss, float* dimg, float* dtxt, double* dscale_part, void* workspace,
+                             size_t ws_bytes, void* stream) {
+  if (!shape_ok(b, d, dtype) || !shard_ok(b, r0, bs)) return INFCL_ERR_INVALID;
+  if (!aligned(img, 16) || !aligned(txt, 16) || !aligned(scale, 4) || !aligned(lse_r, 16) || !aligned(lse_c, 16) ||
+      !aligned(aux, 16) || !aligned(dimg, 16) || !aligned(dtxt, 16) || !aligned(dscale_part, 8) ||
+      !aligned(workspace, 256))
+    return INFCL_ERR_INVALID;
+  if (dloss != nullptr && ((uintptr_t)dloss % 4) != 0) return INFCL_ERR_INVALID;
+  if (!shape_supported(b, d, dtype)) return INFCL_ERR_UNSUPPORTED;
+  const Layout L = make_layout(b);
+  if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
+  char* ws = (char*)workspace;
+  int rc = infcl::launch_bwd(img, txt, b, d, dtype, r0, bs, scale, lse_r, lse_c, aux, dloss, dimg, dtxt, nullptr,
+                             dscale_part, (float*)(ws + L.lse2), (double*)(ws + L.bwd_part), (float*)(ws + L.g16),
                              (hipStream_t)stream);
   if (rc == 2) return INFCL_ERR_UNSUPPORTED;
   return rc == 0 ? INFCL_OK : INFCL_ERR_HIP;

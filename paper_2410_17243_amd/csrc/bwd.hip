@@ -88,11 +88,12 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
   const int l32 = lane & 31, h = lane >> 5;
   const int64_t b = p.b;
-  const int64_t own0 = (int64_t)blockIdx.x * kBwdBM + 32 * wave;  // this wave's first own row
-  const int64_t iown = own0 + l32;                                // this lane's own row
-  const bool own_ok = iown < b;
-  const int64_t irow = own_ok ? iown : b - 1;
-  const bool wave_rows_ok = own0 + 32 <= b;
+  const int64_t wg0 = p.own_off + (int64_t)blockIdx.x * kBwdBM;  // own_off is a multiple of 32
+  const int64_t own0 = wg0 + 32 * wave;                            // this wave's first own row
+  const int64_t iown = own0 + l32;                                 // this lane's own row
+  const bool own_ok = iown < p.own_end;
+  const int64_t irow = own_ok ? iown : p.own_end - 1;
+  const bool wave_rows_ok = own0 + 32 <= p.own_end;
   const int ntile = (int)((b + kBwdBN - 1) / kBwdBN);
 
   const float s = p.scale[0];
@@ -481,27 +482,26 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
 
     // ---- write dOwn: lane holds feature l32 of a 32-feature block, rows 8(r>>2)+4h+(r&3)
     if constexpr (ES == 2) {
-      const int64_t wg0 = (int64_t)blockIdx.x * kBwdBM;
-      const bool all_ok = wg0 + kBwdBM <= b;
+      const bool all_ok = wg0 + kBwdBM <= p.own_end;
 #pragma unroll
       for (int ob = 0; ob < 4; ++ob) {
-        float* dst = p.dOwn + (wg0 + 32 * ob + 4 * h) * D + 32 * (pass * FB + wave * FBW) + l32;
+        float* dst = p.dOwn + (wg0 - p.own_off + 32 * ob + 4 * h) * D + 32 * (pass * FB + wave * FBW) + l32;
 #pragma unroll
         for (int fbw = 0; fbw < FBW; ++fbw)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int64_t row = wg0 + 32 * ob + 8 * (r >> 2) + 4 * h + (r & 3);
-            if (all_ok || row < b) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fbw] = kfin * dacc[ob * FBW + fbw][r];
+            if (all_ok || row < p.own_end) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fbw] = kfin * dacc[ob * FBW + fbw][r];
           }
       }
     } else {
-      float* dst = p.dOwn + (own0 + 4 * h) * D + 32 * pass * FB + l32;
+      float* dst = p.dOwn + (own0 - p.own_off + 4 * h) * D + 32 * pass * FB + l32;
 #pragma unroll
       for (int fb = 0; fb < FB; ++fb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int64_t row = own0 + 8 * (r >> 2) + 4 * h + (r & 3);
-          if (wave_rows_ok || row < b) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fb] = kfin * dacc[fb][r];
+          if (wave_rows_ok || row < p.own_end) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fb] = kfin * dacc[fb][r];
         }
     }
     // the next pass reuses the tile buffers
@@ -518,9 +518,10 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   if (threadIdx.x == 0) p.ds_part[blockIdx.x] = red[0];
 }
 
-// dscale = dloss / (2b) * (sum of both launches' partials), fixed order
+// dscale = dloss / (2b) * (sum of both launches' partials), fixed order; into
+// dscale (fp32) and/or dscale64 (fp64), whichever is given
 __global__ void __launch_bounds__(256) dscale_finish(const double* part, int64_t n, int64_t b, const float* dloss,
-                                                     float* dscale) {
+                                                     float* dscale, double* dscale64) {
   __shared__ double red[256];
   double s = 0.0;
   for (int64_t k = threadIdx.x; k < n; k += 256) s += part[k];
@@ -532,7 +533,9 @@ __global__ void __launch_bounds__(256) dscale_finish(const double* part, int64_t
   }
   if (threadIdx.x == 0) {
     const double dl = dloss ? (double)dloss[0] : 1.0;
-    *dscale = (float)(red[0] * dl / (2.0 * (double)b));
+    const double v = red[0] * dl / (2.0 * (double)b);
+    if (dscale) *dscale = (float)v;
+    if (dscale64) *dscale64 = v;
   }
 }
 
@@ -667,16 +670,21 @@ __global__ void __launch_bounds__(256) lse_to_log2(const float* lse_r, const flo
 }
 
 bool bwd_wide_supported(int64_t d, int dtype);
-int bwd_wide_workgroups(int64_t b);
+int bwd_wide_workgroups(int64_t nown);
 int launch_bwd_wide(const BwdParams& p, int nwg, bool f16, hipStream_t stream);
 
 // Backward: 16-bit inputs with d = 768 or 1024 take the single-pass wide-row sweep
-// (64 own rows per workgroup), everything else the 128-row sweep above.
-int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale,
-               const float* lse_r, const float* lse_c, const float* aux, const float* dloss, float* dimg, float* dtxt,
-               float* dscale, float* lse2, double* ds_part, float* g16, hipStream_t stream) {
+// (64 own rows per workgroup), everything else the 128-row sweep above.  Own
+// rows are [r0, r0 + nrows) of both sides (all b for the whole batch; a
+// shard's samples otherwise, with dimg/dtxt [nrows, d]); lse_r, lse_c and aux
+// cover all b samples.  dscale (fp32) and/or dscale64 (fp64) receive this
+// call's share, dloss/(2b) times its partial sums.
+int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, int64_t r0, int64_t nrows,
+               const float* scale, const float* lse_r, const float* lse_c, const float* aux, const float* dloss,
+               float* dimg, float* dtxt, float* dscale, double* dscale64, float* lse2, double* ds_part, float* g16,
+               hipStream_t stream) {
   const bool wide = bwd_wide_supported(d, dtype);
-  const int nwg = wide ? bwd_wide_workgroups(b) : (int)((b + kBwdBM - 1) / kBwdBM);
+  const int nwg = wide ? bwd_wide_workgroups(nrows) : (int)((nrows + kBwdBM - 1) / kBwdBM);
   auto launch = [&](const BwdParams& q) {
     if (wide) return launch_bwd_wide(q, nwg, dtype == 2, stream);
     if (dtype == 0) return launch_bwd_t<__bf16>(q, nwg, stream);
@@ -700,6 +708,8 @@ int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype
   p.scale = scale;
   p.udiag = aux + 2 * b;
   p.dloss = dloss;
+  p.own_off = r0;
+  p.own_end = r0 + nrows;
   // launch 1: own = image rows (dimg), swept = text rows
   p.own = img;
   p.swept = txt;
@@ -723,7 +733,7 @@ int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype
   rc = launch(p);
   if (rc) return rc;
   hipLaunchKernelGGL(dscale_finish, dim3(1), dim3(256), 0, stream, (const double*)ds_part, (int64_t)2 * nwg, b,
-                     dloss, dscale);
+                     dloss, dscale, dscale64);
   return hipGetLastError() == hipSuccess ? 0 : 1;
 }
 

@@ -16,7 +16,8 @@ struct BwdParams {
   const float* ell_swept;   // [b]
   const float* udiag;       // [b]  <img_i, txt_i>
   const float* dloss;       // device scalar or nullptr (= 1)
-  float* dOwn;              // [b, d]
+  int64_t own_off, own_end;  // own rows [own_off, own_end) (a shard; 0 and b for the whole batch)
+  float* dOwn;              // [own_end - own_off, d], by own row - own_off
   double* ds_part;          // [gridDim.x]
   const float* g16;         // fp16 inputs: (alpha, 1/alpha), the power of two G' is scaled by
 };

@@ -60,12 +60,12 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
   const int ob = wave >> 1, kh = wave & 1;  // own block, feature half of GEMM1
   const int l32 = lane & 31, h = lane >> 5;
   const int64_t b = p.b;
-  const int64_t wg0 = (int64_t)blockIdx.x * kWideBM;
-  const int64_t own0 = wg0 + 32 * ob;  // this wave's own block
+  const int64_t wg0 = p.own_off + (int64_t)blockIdx.x * kWideBM;  // own_off is a multiple of 32
+  const int64_t own0 = wg0 + 32 * ob;                              // this wave's own block
   const int64_t iown = own0 + l32;
-  const bool own_ok = iown < b;
-  const int64_t irow = own_ok ? iown : b - 1;
-  const bool wave_rows_ok = own0 + 32 <= b;
+  const bool own_ok = iown < p.own_end;
+  const int64_t irow = own_ok ? iown : p.own_end - 1;
+  const bool wave_rows_ok = own0 + 32 <= p.own_end;
   const int ntile = (int)((b + kBwdBN - 1) / kBwdBN);
 
   const float s = p.scale[0];
@@ -262,16 +262,16 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
 
   // ---- write dOwn: accumulator dacc[o2 FBW + fbw] lane holds feature l32 of
   // block (wave FBW + fbw), rows 8(r>>2) + 4h + (r&3) of own block o2
-  const bool all_ok = wg0 + kWideBM <= b;
+  const bool all_ok = wg0 + kWideBM <= p.own_end;
 #pragma unroll
   for (int o2 = 0; o2 < 2; ++o2) {
-    float* dst = p.dOwn + (wg0 + 32 * o2 + 4 * h) * D + 32 * (wave * FBW) + l32;
+    float* dst = p.dOwn + (wg0 - p.own_off + 32 * o2 + 4 * h) * D + 32 * (wave * FBW) + l32;
 #pragma unroll
     for (int fbw = 0; fbw < FBW; ++fbw)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int64_t row = wg0 + 32 * o2 + 8 * (r >> 2) + 4 * h + (r & 3);
-        if (all_ok || row < b) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fbw] = kfin * dacc[o2 * FBW + fbw][r];
+        if (all_ok || row < p.own_end) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fbw] = kfin * dacc[o2 * FBW + fbw][r];
       }
   }
 
@@ -287,7 +287,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
 
 bool bwd_wide_supported(int64_t d, int dtype) { return (dtype == 0 || dtype == 2) && (d == 768 || d == 1024); }
 
-int bwd_wide_workgroups(int64_t b) { return (int)((b + kWideBM - 1) / kWideBM); }
+int bwd_wide_workgroups(int64_t nown) { return (int)((nown + kWideBM - 1) / kWideBM); }
 
 int launch_bwd_wide(const BwdParams& p, int nwg, bool f16, hipStream_t stream) {
   switch (p.d) {

@@ -38,13 +38,15 @@ struct FwdParams {
   const void* txt;  // rows j, [b, d]
   int64_t b, d;
   const float* scale;
-  float* rowR;  // [Pc * 4][b]   per (column group, wave) partial row pairs
+  float* rowR;  // [Pc * 4][rstride]   per (column group, wave) partial row pairs, by own row - r0
   float* rowL;
   float* colR;  // [Pr][b]       per row group partial column pairs
   float* colL;
   float* udiag;  // [b]  <img_i, txt_i> as accumulated by the MFMA
   int Pr, Pc;
   int nRT, nCT;
+  int64_t r0, rend;  // own rows [r0, rend) (a shard of the batch; 0 and b for the whole batch)
+  int64_t rstride;   // rend - r0
 };
 
 constexpr int kFwdBI = 64;    // rows i per workgroup tile
@@ -81,7 +83,7 @@ template <typename TIN>
 __device__ __forceinline__ void fwd_stage_dma(const FwdParams& p, const FwdDmaOffsets& o, int64_t i0, int64_t j0,
                                               int st, INFCL_LDS char* buf, int wave) {
   const int64_t b = p.b, rowb = p.d * (int64_t)sizeof(TIN);
-  const u32x4 ri = rsrc_words((const char*)p.img + i0 * rowb, (b - i0) * rowb);
+  const u32x4 ri = rsrc_words((const char*)p.img + i0 * rowb, (p.rend - i0) * rowb);
   const u32x4 rt = rsrc_words((const char*)p.txt + j0 * rowb, (b - j0) * rowb);
   const uint32_t soff = (uint32_t)st * 128u;
 #pragma unroll
@@ -341,17 +343,17 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep(FwdParams p) {
 
   const FwdDmaOffsets dmo = fwd_dma_offsets(p.d, (int)sizeof(TIN), wave, lane);
   int rr = 0, cc = 0;  // position of the current tile in this workgroup's (row, column) sweep
-  fwd_stage_dma<TIN>(p, dmo, (int64_t)q * kFwdBI, (int64_t)ct_lo * kFwdBJ, 0, lds0, wave);
+  fwd_stage_dma<TIN>(p, dmo, p.r0 + (int64_t)q * kFwdBI, (int64_t)ct_lo * kFwdBJ, 0, lds0, wave);
   wait_dma();
   __syncthreads();
 
   for (int tau = 0; tau < ntile; ++tau) {
-    const int64_t i0 = (int64_t)(q + rr * p.Pr) * kFwdBI;
+    const int64_t i0 = p.r0 + (int64_t)(q + rr * p.Pr) * kFwdBI;
     const int64_t j0 = (int64_t)(ct_lo + cc) * kFwdBJ;
     const bool has_next = tau + 1 < ntile;
     const int nrr = cc + 1 == ncol ? rr + 1 : rr;
     const int ncc = cc + 1 == ncol ? 0 : cc + 1;
-    const int64_t ni0 = (int64_t)(q + nrr * p.Pr) * kFwdBI;
+    const int64_t ni0 = p.r0 + (int64_t)(q + nrr * p.Pr) * kFwdBI;
     const int64_t nj0 = (int64_t)(ct_lo + ncc) * kFwdBJ;
 
     f32x16 acc[2][2];
@@ -380,23 +382,27 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep(FwdParams p) {
 
     // the next tile's first stage is in flight while the epilogue runs
     const bool diag = j0 < i0 + kFwdBI && i0 < j0 + kFwdBJ;
-    const bool special = diag || (i0 + kFwdBI > b) || (j0 + kFwdBJ > b);
+    const bool special = diag || (i0 + kFwdBI > p.rend) || (j0 + kFwdBJ > b);
     if (special) {
       const int64_t jw = j0 + 64 * wave + 4 * h;
       if (diag) {
-        // the diagonal entry of row i sits in block mb == nb of one lane of one wave
+        // the diagonal entry of row i sits in one lane of one wave, in block
+        // mb == nb when i0 - j0 is a multiple of 64 (whole batch), in either
+        // block for a shard starting at a multiple of 32
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb) {
           const int64_t i = i0 + 32 * nb + l32;
           float dv = 0.f;
           bool has = false;
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const bool hit = jw + 32 * nb + 8 * (r >> 2) + (r & 3) == i;
-            dv = hit ? acc[nb][nb][r] : dv;
-            has |= hit;
-          }
-          if (has && i < b) p.udiag[i] = dv;
+          for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const bool hit = jw + 32 * mb + 8 * (r >> 2) + (r & 3) == i;
+              dv = hit ? acc[mb][nb][r] : dv;
+              has |= hit;
+            }
+          if (has && i < p.rend) p.udiag[i] = dv;
         }
       }
       // scaled exponents, -inf for the diagonal and for rows/columns past b
@@ -408,7 +414,7 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep(FwdParams p) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int64_t j = jw + 32 * mb + 8 * (r >> 2) + (r & 3);
-            const bool ok = i < b && j < b && i != j;
+            const bool ok = i < p.rend && j < b && i != j;
             acc[mb][nb][r] = ok ? acc[mb][nb][r] * k2 : ninf;
           }
         }
@@ -424,8 +430,8 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep(FwdParams p) {
         float R = rowR[nb], L = rowL[nb];
         lse2_merge(R, L, shfl_xor(rowR[nb], 32), shfl_xor(rowL[nb], 32));
         const int64_t i = i0 + 32 * nb + l32;
-        if (h == 0 && i < b) {
-          const int64_t slot = (int64_t)(g * 4 + wave) * b + i;
+        if (h == 0 && i < p.rend) {
+          const int64_t slot = (int64_t)(g * 4 + wave) * p.rstride + (i - p.r0);
           p.rowR[slot] = R;
           p.rowL[slot] = L;
         }
@@ -444,30 +450,37 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep(FwdParams p) {
 }
 
 // ---------------------------------------------------------------- finalize
+// Per-sample terms of samples [r0, r0 + n) (all b for the whole batch, a
+// shard's own samples otherwise).  Sample r0 + t takes its row pair from the
+// nrowpart partials at rowR/rowL[k rstride + t] and its column pair from the
+// ncolpart partials at colR/colL[k cstride + t].
 struct FinParams {
-  int64_t b;
+  int64_t r0, n;
   const float* scale;
   const float* rowR;
   const float* rowL;
   int nrowpart;
+  int64_t rstride;
   const float* colR;
   const float* colL;
   int ncolpart;
-  const float* udiag;
-  float* lse_r;
-  float* lse_c;
-  float* aux;       // [3b]
-  double* partial;  // [gridDim.x]
+  int64_t cstride;
+  const float* udiag;  // [b], by sample index
+  float* lse_r;        // [n]
+  float* lse_c;        // [n]
+  float* aux;          // [3n]: l^r, l^c, u_ii
+  double* partial;     // [gridDim.x]
 };
 
-__device__ __forceinline__ double merge_parts(const float* R, const float* L, int n, int64_t b, int64_t i) {
+// natural-log log-sum-exp of n base-2 partial pairs (R, l) at R/L[k stride + t]
+__device__ __forceinline__ double merge_parts(const float* R, const float* L, int n, int64_t stride, int64_t t) {
   double M = -__builtin_inf();
-  for (int k = 0; k < n; ++k) M = fmax(M, (double)R[(int64_t)k * b + i]);
+  for (int k = 0; k < n; ++k) M = fmax(M, (double)R[(int64_t)k * stride + t]);
   if (M == -__builtin_inf()) return -__builtin_inf();
   double S = 0.0;
   for (int k = 0; k < n; ++k) {
-    double r = R[(int64_t)k * b + i];
-    if (r != -__builtin_inf()) S += (double)L[(int64_t)k * b + i] * exp2(r - M);
+    double r = R[(int64_t)k * stride + t];
+    if (r != -__builtin_inf()) S += (double)L[(int64_t)k * stride + t] * exp2(r - M);
   }
   return (M + log2(S)) * 0.6931471805599453;  // natural-log LSE over the off-diagonal entries
 }
@@ -479,21 +492,21 @@ __device__ __forceinline__ double softplus64(double z) {
 
 __global__ void __launch_bounds__(256) fwd_finalize(FinParams p) {
   __shared__ double red[256];
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
   double contrib = 0.0;
-  if (i < p.b) {
+  if (t < p.n) {
     const double s = (double)p.scale[0];
-    const double u = (double)p.udiag[i];
+    const double u = (double)p.udiag[p.r0 + t];
     const double x = s * u;
-    const double offr = merge_parts(p.rowR, p.rowL, p.nrowpart, p.b, i);
-    const double offc = merge_parts(p.colR, p.colL, p.ncolpart, p.b, i);
+    const double offr = merge_parts(p.rowR, p.rowL, p.nrowpart, p.rstride, t);
+    const double offc = merge_parts(p.colR, p.colL, p.ncolpart, p.cstride, t);
     const double er = softplus64(offr - x);  // r_i - x_ii, cancellation-free
     const double ec = softplus64(offc - x);
-    p.lse_r[i] = (float)(x + er);
-    p.lse_c[i] = (float)(x + ec);
-    p.aux[i] = (float)er;
-    p.aux[p.b + i] = (float)ec;
-    p.aux[2 * p.b + i] = (float)u;
+    p.lse_r[t] = (float)(x + er);
+    p.lse_c[t] = (float)(x + ec);
+    p.aux[t] = (float)er;
+    p.aux[p.n + t] = (float)ec;
+    p.aux[2 * p.n + t] = (float)u;
     contrib = er + ec;
   }
   red[threadIdx.x] = contrib;
@@ -503,6 +516,26 @@ __global__ void __launch_bounds__(256) fwd_finalize(FinParams p) {
     __syncthreads();
   }
   if (threadIdx.x == 0) p.partial[blockIdx.x] = red[0];
+}
+
+// Sharded forward: one base-2 pair per column j in [0, b) over this shard's
+// rows, merged from the ncolpart row-group partials (colR/colL[k b + j]) in a
+// fixed order: out[j] = R, out[b + j] = l.  This is what the column owner
+// receives from every shard.
+__global__ void __launch_bounds__(256) fwd_col_pairs(const float* colR, const float* colL, int ncolpart, int64_t b,
+                                                     float* out) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (j >= b) return;
+  float M = -__builtin_inff();
+  for (int k = 0; k < ncolpart; ++k) M = fmaxf(M, colR[(int64_t)k * b + j]);
+  double S = 0.0;
+  if (M != -__builtin_inff())
+    for (int k = 0; k < ncolpart; ++k) {
+      const float r = colR[(int64_t)k * b + j];
+      if (r != -__builtin_inff()) S += (double)colL[(int64_t)k * b + j] * exp2((double)r - (double)M);
+    }
+  out[j] = M;
+  out[b + j] = (float)S;
 }
 
 // Fixed-order sum of `n` fp64 partials, times `mul`; one workgroup.
@@ -526,13 +559,23 @@ __global__ void __launch_bounds__(256) sum_partials(const double* part, int64_t 
 
 // ------------------------------------------------------------ host launchers
 bool fwd2_supported(int64_t d, int dtype);
-void fwd2_grid(int64_t b, int* Pr, int* Pc);
-int launch_fwd2(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale, float* rowR,
-                float* rowL, float* colR, float* colL, float* udiag, float* ref2, hipStream_t stream);
+void fwd2_grid(int64_t b, int64_t nrows, int* Pr, int* Pc);
+int launch_fwd2(const void* img, const void* txt, int64_t b, int64_t d, int dtype, int64_t r0, int64_t nrows,
+                const float* scale, float* rowR, float* rowL, float* colR, float* colL, float* udiag, float* ref2,
+                hipStream_t stream);
 
-static int launch_fwd1(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale,
-                       hipStream_t stream, int Pr, int Pc, float* rowR, float* rowL, float* colR, float* colL,
-                       float* udiag) {
+// Grid of the streamed-tiles sweep for nrows own rows against b columns: Pc
+// column groups (one per XCD when there are enough column tiles) times Pr row
+// groups, about two workgroups per compute unit.
+void fwd1_grid(int64_t b, int64_t nrows, int* Pr, int* Pc) {
+  const int64_t nRT = (nrows + kFwdBI - 1) / kFwdBI, nCT = (b + kFwdBJ - 1) / kFwdBJ;
+  *Pc = (int)(nCT < 8 ? nCT : 8);
+  *Pr = (int)(nRT < 64 ? nRT : 64);
+}
+
+static int launch_fwd1(const void* img, const void* txt, int64_t b, int64_t d, int dtype, int64_t r0, int64_t nrows,
+                       const float* scale, hipStream_t stream, float* rowR, float* rowL, float* colR, float* colL,
+                       float* udiag, int* nrowpart, int* ncolpart) {
   FwdParams p;
   p.img = img;
   p.txt = txt;
@@ -544,11 +587,15 @@ static int launch_fwd1(const void* img, const void* txt, int64_t b, int64_t d, i
   p.colR = colR;
   p.colL = colL;
   p.udiag = udiag;
-  p.Pr = Pr;
-  p.Pc = Pc;
-  p.nRT = (int)((b + kFwdBI - 1) / kFwdBI);
+  fwd1_grid(b, nrows, &p.Pr, &p.Pc);
+  p.nRT = (int)((nrows + kFwdBI - 1) / kFwdBI);
   p.nCT = (int)((b + kFwdBJ - 1) / kFwdBJ);
-  dim3 grid(Pr * Pc);
+  p.r0 = r0;
+  p.rend = r0 + nrows;
+  p.rstride = nrows;
+  *nrowpart = p.Pc * 4;
+  *ncolpart = p.Pr;
+  dim3 grid(p.Pr * p.Pc);
   if (dtype == 0)
     hipLaunchKernelGGL(fwd_sweep<__bf16>, grid, dim3(256), 0, stream, p);
   else if (dtype == 2)
@@ -558,52 +605,104 @@ static int launch_fwd1(const void* img, const void* txt, int64_t b, int64_t d, i
   return hipGetLastError() == hipSuccess ? 0 : 1;
 }
 
-static int launch_finalize(int64_t b, const float* scale, float* loss, double* loss64, float* lse_r, float* lse_c,
-                           float* aux, const float* rowR, const float* rowL, int nrowpart, const float* colR,
-                           const float* colL, int ncolpart, const float* udiag, double* partial, hipStream_t stream) {
+// The sweep over own rows [r0, r0 + nrows) against all b columns: 16-bit
+// inputs with d <= 512 take the resident-rows sweep, everything else the
+// streamed-tiles sweep above.  Both leave partial pairs: nrowpart per own row
+// (stride nrows, by row - r0) and ncolpart per column (stride b).
+static int launch_sweep(const void* img, const void* txt, int64_t b, int64_t d, int dtype, int64_t r0, int64_t nrows,
+                        const float* scale, float* rowR, float* rowL, float* colR, float* colL, float* udiag,
+                        float* ref2, hipStream_t stream, int* nrowpart, int* ncolpart) {
+  if (fwd2_supported(d, dtype)) {
+    int Pr2 = 0, Pc2 = 0;
+    fwd2_grid(b, nrows, &Pr2, &Pc2);
+    *nrowpart = Pc2;
+    *ncolpart = Pr2;
+    return launch_fwd2(img, txt, b, d, dtype, r0, nrows, scale, rowR, rowL, colR, colL, udiag, ref2, stream);
+  }
+  return launch_fwd1(img, txt, b, d, dtype, r0, nrows, scale, stream, rowR, rowL, colR, colL, udiag, nrowpart,
+                     ncolpart);
+}
+
+// Row partial count of the sweep over nrows own rows (what the finalize of a
+// shard has to merge).
+int sweep_rowparts(int64_t b, int64_t d, int dtype, int64_t nrows) {
+  int Pr = 0, Pc = 0;
+  if (fwd2_supported(d, dtype)) {
+    fwd2_grid(b, nrows, &Pr, &Pc);
+    return Pc;
+  }
+  fwd1_grid(b, nrows, &Pr, &Pc);
+  return Pc * 4;
+}
+
+static int launch_finalize(int64_t r0, int64_t n, double loss_mul, const float* scale, float* loss, double* loss64,
+                           float* lse_r, float* lse_c, float* aux, const float* rowR, const float* rowL, int nrowpart,
+                           int64_t rstride, const float* colR, const float* colL, int ncolpart, int64_t cstride,
+                           const float* udiag, double* partial, hipStream_t stream) {
   FinParams f;
-  f.b = b;
+  f.r0 = r0;
+  f.n = n;
   f.scale = scale;
   f.rowR = rowR;
   f.rowL = rowL;
   f.nrowpart = nrowpart;
+  f.rstride = rstride;
   f.colR = colR;
   f.colL = colL;
   f.ncolpart = ncolpart;
+  f.cstride = cstride;
   f.udiag = udiag;
   f.lse_r = lse_r;
   f.lse_c = lse_c;
   f.aux = aux;
   f.partial = partial;
-  int nfin = (int)((b + 255) / 256);
+  int nfin = (int)((n + 255) / 256);
   hipLaunchKernelGGL(fwd_finalize, dim3(nfin), dim3(256), 0, stream, f);
   if (hipGetLastError() != hipSuccess) return 1;
-  hipLaunchKernelGGL(sum_partials, dim3(1), dim3(256), 0, stream, (const double*)partial, (int64_t)nfin,
-                     1.0 / (2.0 * (double)b), loss, loss64);
+  hipLaunchKernelGGL(sum_partials, dim3(1), dim3(256), 0, stream, (const double*)partial, (int64_t)nfin, loss_mul,
+                     loss, loss64);
   return hipGetLastError() == hipSuccess ? 0 : 1;
 }
 
-// Forward: bf16 with d <= 512 takes the resident-rows sweep, everything else
-// the streamed-tiles sweep above; both leave partial pairs that the finalize
-// merges.
+// Forward over the whole batch: the sweep over all rows, then the finalize of
+// every sample and the loss.
 int launch_fwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale, float* loss,
-               double* loss64, float* lse_r, float* lse_c, float* aux, char* ws, hipStream_t stream, int Pr, int Pc,
-               float* rowR, float* rowL, float* colR, float* colL, float* udiag, float* ref2, double* partial) {
-  (void)ws;
-  int nrowpart = Pc * 4, ncolpart = Pr;
-  if (fwd2_supported(d, dtype)) {
-    int Pr2 = 0, Pc2 = 0;
-    fwd2_grid(b, &Pr2, &Pc2);
-    const int rc = launch_fwd2(img, txt, b, d, dtype, scale, rowR, rowL, colR, colL, udiag, ref2, stream);
-    if (rc != 0) return rc;
-    nrowpart = Pc2;
-    ncolpart = Pr2;
-  } else {
-    const int rc = launch_fwd1(img, txt, b, d, dtype, scale, stream, Pr, Pc, rowR, rowL, colR, colL, udiag);
-    if (rc != 0) return rc;
-  }
-  return launch_finalize(b, scale, loss, loss64, lse_r, lse_c, aux, rowR, rowL, nrowpart, colR, colL, ncolpart, udiag,
-                         partial, stream);
+               double* loss64, float* lse_r, float* lse_c, float* aux, hipStream_t stream, float* rowR, float* rowL,
+               float* colR, float* colL, float* udiag, float* ref2, double* partial) {
+  int nrowpart = 0, ncolpart = 0;
+  const int rc =
+      launch_sweep(img, txt, b, d, dtype, 0, b, scale, rowR, rowL, colR, colL, udiag, ref2, stream, &nrowpart, &ncolpart);
+  if (rc != 0) return rc;
+  return launch_finalize(0, b, 1.0 / (2.0 * (double)b), scale, loss, loss64, lse_r, lse_c, aux, rowR, rowL, nrowpart,
+                         b, colR, colL, ncolpart, b, udiag, partial, stream);
+}
+
+// Sharded forward, local part: the sweep over own rows [r0, r0 + nrows), row
+// partials left in the workspace, and one base-2 pair per column over the own
+// rows written to colpair ([2b]: R then l).
+int launch_fwd_shard(const void* img, const void* txt, int64_t b, int64_t d, int dtype, int64_t r0, int64_t nrows,
+                     const float* scale, float* colpair, hipStream_t stream, float* rowR, float* rowL, float* colR,
+                     float* colL, float* udiag, float* ref2) {
+  int nrowpart = 0, ncolpart = 0;
+  const int rc = launch_sweep(img, txt, b, d, dtype, r0, nrows, scale, rowR, rowL, colR, colL, udiag, ref2, stream,
+                              &nrowpart, &ncolpart);
+  if (rc != 0) return rc;
+  hipLaunchKernelGGL(fwd_col_pairs, dim3((unsigned)((b + 255) / 256)), dim3(256), 0, stream, (const float*)colR,
+                     (const float*)colL, ncolpart, b, colpair);
+  return hipGetLastError() == hipSuccess ? 0 : 1;
+}
+
+// Sharded forward, owner part: the per-sample terms of own samples [r0, r0 +
+// nrows) from the row partials of launch_fwd_shard and the nparts column pairs
+// received for the own columns (colpairs: [nparts][2 nrows], R then l), and
+// this shard's share of the loss, sum of (l^r + l^c) / (2b), into loss_part.
+int launch_fwd_shard_finish(int64_t b, int64_t d, int dtype, int64_t r0, int64_t nrows, int64_t nparts,
+                            const float* colpairs, const float* scale, float* lse_r, float* lse_c, float* aux,
+                            double* loss_part, hipStream_t stream, const float* rowR, const float* rowL,
+                            const float* udiag, double* partial) {
+  const int nrowpart = sweep_rowparts(b, d, dtype, nrows);
+  return launch_finalize(r0, nrows, 1.0 / (2.0 * (double)b), scale, nullptr, loss_part, lse_r, lse_c, aux, rowR, rowL,
+                         nrowpart, nrows, colpairs, colpairs + nrows, (int)nparts, 2 * nrows, udiag, partial, stream);
 }
 
 }  // namespace infcl

@@ -46,12 +46,14 @@ struct Fwd2Params {
   int64_t b;
   const float* scale;
   const float* ref2;  // [b]  s log2(e) <img_i, txt_i>
-  float* rowR;        // [Pc][b]
+  float* rowR;        // [Pc][rstride]  indexed by own row - r0
   float* rowL;
+  int r0, rend;     // own rows [r0, rend) (a shard of the batch; 0 and b for the whole batch)
+  int64_t rstride;  // rend - r0
   float* colR;  // [Pr][b]
   float* colL;
   int Pr, Pc;
-  int nRB;  // row blocks of 128
+  int nRB;  // row blocks of kF2BM own rows
   int nCT;  // column tiles of 32
 };
 
@@ -209,12 +211,12 @@ __global__ void __launch_bounds__(64 * kF2NW, 2) fwd_sweep2(Fwd2Params p) {
 
   for (int rb = q; rb < p.nRB; rb += p.Pr) {
     const bool first_rb = rb == q;
-    const int own0 = rb * kF2BM + 32 * wave;
+    const int own0 = p.r0 + rb * kF2BM + 32 * wave;  // r0 is a multiple of 32: own blocks stay tile-aligned
     const int iown = own0 + l32;
-    const bool own_ok = iown < b;
-    const int irow = own_ok ? iown : b - 1;
-    const bool wave_rows_ok = own0 + 32 <= b;
-    const bool wave_any_row = own0 < b;
+    const bool own_ok = iown < p.rend;
+    const int irow = own_ok ? iown : p.rend - 1;
+    const bool wave_rows_ok = own0 + 32 <= p.rend;
+    const bool wave_any_row = own0 < p.rend;
 
     bf16x8 ownf[KS];
     {
@@ -458,8 +460,8 @@ __global__ void __launch_bounds__(64 * kF2NW, 2) fwd_sweep2(Fwd2Params p) {
       float R = rowR, L = rowL;
       lse2_merge(R, L, shfl_xor(rowR, 32), shfl_xor(rowL, 32));
       if (h == 0 && own_ok) {
-        p.rowR[(int64_t)g * b + iown] = R;
-        p.rowL[(int64_t)g * b + iown] = L;
+        p.rowR[(int64_t)g * p.rstride + (iown - p.r0)] = R;
+        p.rowL[(int64_t)g * p.rstride + (iown - p.r0)] = L;
       }
     }
     // column pairs stored in this row block are read by the next one's DMA
@@ -482,16 +484,17 @@ bool fwd2_supported(int64_t d, int dtype) {
   return (dtype == 0 || dtype == 2) && (d == 128 || d == 256 || d == 384 || d == 512);
 }
 
-// Grid of the resident-rows forward for b samples.
-void fwd2_grid(int64_t b, int* Pr, int* Pc) {
-  const int64_t nRB = (b + kF2BM - 1) / kF2BM, nCT = (b + kSweepBN - 1) / kSweepBN;
+// Grid of the resident-rows forward for nrows own rows against b columns.
+void fwd2_grid(int64_t b, int64_t nrows, int* Pr, int* Pc) {
+  const int64_t nRB = (nrows + kF2BM - 1) / kF2BM, nCT = (b + kSweepBN - 1) / kSweepBN;
   *Pc = (int)(nCT < 8 ? nCT : 8);
   const int64_t pmax = 256 / kF2NW;  // P_r P_c <= 2048 / NW: two workgroups per CU with 4 waves, one with 8
   *Pr = (int)(nRB < pmax ? nRB : pmax);
 }
 
-int launch_fwd2(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale, float* rowR,
-                float* rowL, float* colR, float* colL, float* udiag, float* ref2, hipStream_t stream) {
+int launch_fwd2(const void* img, const void* txt, int64_t b, int64_t d, int dtype, int64_t r0, int64_t nrows,
+                const float* scale, float* rowR, float* rowL, float* colR, float* colL, float* udiag, float* ref2,
+                hipStream_t stream) {
   const bool f16 = dtype == 2;
   if (f16)
     hipLaunchKernelGGL(fwd2_diag<true>, dim3((unsigned)((b + 31) / 32)), dim3(256), 0, stream, (const __bf16*)img,
@@ -510,8 +513,11 @@ int launch_fwd2(const void* img, const void* txt, int64_t b, int64_t d, int dtyp
   p.rowL = rowL;
   p.colR = colR;
   p.colL = colL;
-  fwd2_grid(b, &p.Pr, &p.Pc);
-  p.nRB = (int)((b + kF2BM - 1) / kF2BM);
+  p.r0 = (int)r0;
+  p.rend = (int)(r0 + nrows);
+  p.rstride = nrows;
+  fwd2_grid(b, nrows, &p.Pr, &p.Pc);
+  p.nRB = (int)((nrows + kF2BM - 1) / kF2BM);
   p.nCT = (int)((b + kSweepBN - 1) / kSweepBN);
   switch (d) {
     case 128: return launch_fwd2_d<128>(p, f16, stream);

@@ -15,7 +15,8 @@ def lib():
 
 def test_exports_every_declared_function(lib):
     names = infcl.header_functions()
-    assert set(names) == {"infcl_workspace_size", "infcl_fwd", "infcl_bwd", "infcl_status_str"}
+    assert set(names) == {"infcl_workspace_size", "infcl_fwd", "infcl_bwd", "infcl_status_str", "infcl_fwd_shard",
+                          "infcl_fwd_shard_finish", "infcl_bwd_shard"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -91,3 +92,56 @@ def test_fwd_validation(lib, kw, expect):
 ])
 def test_bwd_validation(lib, kw, expect):
     assert _bwd(lib, **kw) == expect
+
+
+# ---------------------------------------------------------------- shard calls
+
+def _fwd_shard(lib, b=1000, d=512, dt=0, r0=0, bs=1000, scale=A, cp=A, ws=A, wsb=1 << 30):
+    return lib.infcl_fwd_shard(A, A, b, d, dt, r0, bs, scale, cp, ws, wsb, None)
+
+
+def _finish(lib, b=1000, d=512, dt=0, r0=0, bs=1000, nparts=2, cps=A, scale=A, lr=A, lc=A, aux=A, lp=A, ws=A,
+            wsb=1 << 30):
+    return lib.infcl_fwd_shard_finish(b, d, dt, r0, bs, nparts, cps, scale, lr, lc, aux, lp, ws, wsb, None)
+
+
+def _bwd_shard(lib, b=1000, d=512, dt=0, r0=0, bs=1000, ds=A, di=A, wsb=1 << 30):
+    return lib.infcl_bwd_shard(A, A, b, d, dt, r0, bs, A, A, A, A, None, di, A, ds, A, wsb, None)
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(r0=16), infcl.INFCL_ERR_INVALID), (dict(r0=-32), infcl.INFCL_ERR_INVALID), (dict(bs=0), infcl.INFCL_ERR_INVALID),
+    (dict(r0=992, bs=9), infcl.INFCL_ERR_INVALID), (dict(cp=A + 4), infcl.INFCL_ERR_INVALID),
+    (dict(cp=None), infcl.INFCL_ERR_INVALID), (dict(d=96), infcl.INFCL_ERR_UNSUPPORTED),
+    (dict(wsb=16), infcl.INFCL_ERR_WORKSPACE),
+])
+def test_fwd_shard_validation(lib, kw, expect):
+    assert _fwd_shard(lib, **kw) == expect
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(nparts=0), infcl.INFCL_ERR_INVALID), (dict(r0=33), infcl.INFCL_ERR_INVALID), (dict(lp=A + 4), infcl.INFCL_ERR_INVALID),
+    (dict(cps=None), infcl.INFCL_ERR_INVALID), (dict(bs=1001), infcl.INFCL_ERR_INVALID),
+    (dict(wsb=16), infcl.INFCL_ERR_WORKSPACE),
+])
+def test_fwd_shard_finish_validation(lib, kw, expect):
+    assert _finish(lib, **kw) == expect
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(r0=8), infcl.INFCL_ERR_INVALID), (dict(ds=A + 4), infcl.INFCL_ERR_INVALID), (dict(di=None), infcl.INFCL_ERR_INVALID),
+    (dict(r0=960, bs=64), infcl.INFCL_ERR_INVALID), (dict(dt=1, d=1024), infcl.INFCL_ERR_UNSUPPORTED),
+    (dict(wsb=16), infcl.INFCL_ERR_WORKSPACE),
+])
+def test_bwd_shard_validation(lib, kw, expect):
+    assert _bwd_shard(lib, **kw) == expect
+
+
+def test_shard_bounds():
+    from paper_2410_17243_amd.shards import shard_bounds
+    for b, n in [(1, 1), (100, 3), (1000, 4), (32768, 8), (4097, 7)]:
+        bd = shard_bounds(b, n)
+        assert bd[0][0] == 0 and sum(bs for _, bs in bd) == b
+        assert all(r0 % 32 == 0 and bs >= 1 for r0, bs in bd)
+        assert all(bd[k][0] + bd[k][1] == bd[k + 1][0] for k in range(len(bd) - 1))
+        assert len(bd) <= n

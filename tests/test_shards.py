@@ -1,0 +1,105 @@
+"""Sharded loss (one GPU's share of a batch sharded over n GPUs), run as n
+shards on one device: against the fp64 oracle at the parity bars, and against
+the whole-batch entry points on the same inputs."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2410_17243_amd as infcl
+from gpu_util import device_inputs, f32_scale, lse_tol, max_rel, run, synth
+from paper_2410_17243_amd.shards import sharded_forward_backward
+
+pytestmark = pytest.mark.gpu
+
+BARS = {"bf16": (1e-3, 2e-2), "f16": (1e-3, 2.5e-3), "f32": (1e-5, 1e-4)}
+
+
+def _sharded(img, txt, dtype, s, n, dloss=1.0):
+    I, T = device_inputs(img, txt, dtype)
+    sc = torch.tensor([s], dtype=torch.float32, device=I.device)
+    dl = torch.tensor([dloss], dtype=torch.float32, device=I.device)
+    out = sharded_forward_backward(I, T, sc, n, dloss=dl)
+    torch.cuda.synchronize()
+    b = I.shape[0]
+    aux = out["aux"].cpu().numpy().astype(np.float64)
+    return {
+        "loss64": float(out["loss64"].item()),
+        "lse_r": out["lse_r"].cpu().numpy().astype(np.float64),
+        "lse_c": out["lse_c"].cpu().numpy().astype(np.float64),
+        "ell_r": aux[:b], "ell_c": aux[b:2 * b], "udiag": aux[2 * b:],
+        "dI": out["dimg"].cpu().numpy().astype(np.float64),
+        "dT": out["dtxt"].cpu().numpy().astype(np.float64),
+        "dscale": float(out["dscale64"].item()),
+        "bounds": out["bounds"],
+    }
+
+
+@pytest.mark.parametrize("b,d,dtype,n", [
+    (1000, 512, "bf16", 3),    # resident-rows forward, 128-row backward
+    (2048, 256, "bf16", 4),
+    (777, 768, "bf16", 2),     # streamed forward, wide backward
+    (1025, 128, "f32", 3),     # fp32 inputs
+    (1500, 512, "f16", 5),     # fp16 inputs
+    (300, 128, "bf16", 10),    # shards of 32 rows and a ragged last one of 12
+])
+def test_sharded_matches_oracle_and_whole_batch(b, d, dtype, n):
+    img, txt = synth.clip_pairs(b, d, 1.0, seed=b + n, dtype=dtype)
+    s = f32_scale(14.29)
+    sh = _sharded(img, txt, dtype, s, n, dloss=0.7)
+    assert len(sh["bounds"]) == n
+    fwd, dI, dT, ds = oracle.forward_backward(synth.as_f64(img, dtype), synth.as_f64(txt, dtype), s, dloss=0.7)
+    loss_tol, grad_tol = BARS[dtype]
+    print(f"n={n}: loss {sh['loss64']:.9e} ref {fwd['loss']:.9e} | dI {max_rel(sh['dI'], dI):.2e} "
+          f"dT {max_rel(sh['dT'], dT):.2e} | ds {sh['dscale']:.6e} ref {ds:.6e}", flush=True)
+    assert sh["loss64"] == pytest.approx(fwd["loss"], rel=loss_tol)
+    assert np.all(np.abs(sh["lse_r"] - fwd["lse_r"]) <= lse_tol(s, d, fwd["lse_r"]))
+    assert np.all(np.abs(sh["lse_c"] - fwd["lse_c"]) <= lse_tol(s, d, fwd["lse_c"]))
+    assert max_rel(sh["dI"], dI) <= grad_tol and max_rel(sh["dT"], dT) <= grad_tol
+    assert abs(sh["dscale"] - ds) <= grad_tol * abs(ds) + 1e-12
+    # the whole-batch entry points on the same inputs: same quantities up to
+    # the order of the column merges
+    whole = run(img, txt, dtype, s, dloss=0.7)
+    assert sh["loss64"] == pytest.approx(whole["loss64"], rel=1e-6)
+    np.testing.assert_allclose(sh["lse_r"], whole["lse_r"], rtol=0, atol=1e-5 * max(1.0, s))
+    np.testing.assert_allclose(sh["lse_c"], whole["lse_c"], rtol=0, atol=1e-5 * max(1.0, s))
+    np.testing.assert_array_equal(sh["udiag"], whole["u_diag"])
+    assert max_rel(sh["dI"], whole["dI"]) <= grad_tol and max_rel(sh["dT"], whole["dT"]) <= grad_tol
+
+
+def test_single_shard_is_the_whole_batch():
+    b, d = 700, 256
+    img, txt = synth.clip_pairs(b, d, 1.0, seed=2, dtype="bf16")
+    s = f32_scale(14.29)
+    sh = _sharded(img, txt, "bf16", s, 1)
+    whole = run(img, txt, "bf16", s)
+    assert sh["bounds"] == [(0, b)]
+    assert sh["loss64"] == pytest.approx(whole["loss64"], rel=1e-9)
+    np.testing.assert_allclose(sh["lse_c"], whole["lse_c"], rtol=0, atol=1e-5 * s)
+    np.testing.assert_array_equal(sh["lse_r"], whole["lse_r"])
+    np.testing.assert_array_equal(sh["ell_r"], whole["ell_r"])
+
+
+def test_sharded_full_size_workload_2():
+    """b = 32768, d = 512 (the benchmark shapes) as 8 shards of 4096 samples,
+    the share of each of 8 GPUs: against the whole-batch result and the
+    invariant <dI, I> = <dT, T> = s * dscale."""
+    cfg = synth.CONFIGS[2]
+    b, d = cfg["b"], cfg["d"]
+    img, txt = synth.clip_pairs(b, d, cfg["sigma"], seed=0, dtype="bf16")
+    s = f32_scale(cfg["scale"])
+    sh = _sharded(img, txt, "bf16", s, 8)
+    assert [bs for _, bs in sh["bounds"]] == [4096] * 8
+    whole = run(img, txt, "bf16", s)
+    print(f"loss sharded {sh['loss64']:.12e} whole {whole['loss64']:.12e}; dI {max_rel(sh['dI'], whole['dI']):.2e}",
+          flush=True)
+    assert sh["loss64"] == pytest.approx(whole["loss64"], rel=1e-6)
+    np.testing.assert_allclose(sh["lse_c"], whole["lse_c"], rtol=0, atol=2e-4)
+    assert max_rel(sh["dI"], whole["dI"]) <= 2e-2 and max_rel(sh["dT"], whole["dT"]) <= 2e-2
+    I = synth.as_f64(img, "bf16")
+    T = synth.as_f64(txt, "bf16")
+    gi = float(np.sum(sh["dI"] * I))
+    gt = float(np.sum(sh["dT"] * T))
+    assert gi == pytest.approx(s * sh["dscale"], rel=2e-2)
+    assert gt == pytest.approx(s * sh["dscale"], rel=2e-2)
