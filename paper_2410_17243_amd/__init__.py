@@ -24,6 +24,7 @@ import re
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libinfcl.so")
 HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "infcl.h")
+ABLATION_HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "infcl_ablation.h")
 
 INFCL_OK, INFCL_ERR_INVALID, INFCL_ERR_UNSUPPORTED, INFCL_ERR_WORKSPACE, INFCL_ERR_HIP = range(5)
 INFCL_BF16, INFCL_F32, INFCL_F16 = 0, 1, 2
@@ -62,6 +63,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.infcl_fwd_shard_finish.restype = ip
     lib.infcl_bwd_shard.argtypes = [vp, vp, i64, i64, ip, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.infcl_bwd_shard.restype = ip
+    lib.infcl_ablation_dt_atomics.argtypes = [vp, i64, i64, i64, vp]
+    lib.infcl_ablation_dt_atomics.restype = ip
     lib.infcl_status_str.argtypes = [ip]
     lib.infcl_status_str.restype = ctypes.c_char_p
     _lib = lib
@@ -152,6 +155,14 @@ def infcl_bwd_shard(img, txt, scale, r0, bs, lse_r, lse_c, aux, dloss, dimg, dtx
                                            _ptr(dscale_part), _ptr(workspace),
                                            workspace.numel() * workspace.element_size(), _stream(img)),
            "infcl_bwd_shard")
+
+
+def infcl_ablation_dt_atomics(dT, bm: int):
+    """The text-gradient update traffic of a single-launch backward (include/infcl_ablation.h)."""
+    b, d = dT.shape
+    rc = load_library().infcl_ablation_dt_atomics(_ptr(dT), b, d, int(bm), _stream(dT))
+    if rc != 0:
+        raise InfclError(rc, "infcl_ablation_dt_atomics")
 
 
 # ------------------------------------------------------------- torch wrappers

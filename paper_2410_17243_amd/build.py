@@ -20,7 +20,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libinfcl.so")
-SOURCES = ["api.hip", "fwd.hip", "fwd2.hip", "bwd.hip", "bwd_wide.hip"]
+SOURCES = ["api.hip", "fwd.hip", "fwd2.hip", "bwd.hip", "bwd_wide.hip", "ablation.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

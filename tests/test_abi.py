@@ -13,6 +13,16 @@ def lib():
     return infcl.load_library()
 
 
+def test_ablation_header_symbol_exported(lib):
+    names = infcl.header_functions(infcl.ABLATION_HEADER_PATH)
+    assert names == ["infcl_ablation_dt_atomics"]
+    assert hasattr(lib, names[0])
+    assert lib.infcl_ablation_dt_atomics(None, 64, 64, 128, None) == 1
+    assert lib.infcl_ablation_dt_atomics(A + 4, 64, 64, 128, None) == 1
+    assert lib.infcl_ablation_dt_atomics(A, 0, 64, 128, None) == 1
+    assert lib.infcl_ablation_dt_atomics(A, 64, 64, 0, None) == 1
+
+
 def test_exports_every_declared_function(lib):
     names = infcl.header_functions()
     assert set(names) == {"infcl_workspace_size", "infcl_fwd", "infcl_bwd", "infcl_status_str", "infcl_fwd_shard",
