@@ -192,7 +192,9 @@ def main():
 
     entries = float(b) * float(b)
     value = entries / (ms_per_step * 1e-3)
-    bwd_launch_ms = sum(bwd_ms) / len(bwd_ms) / 2.0   # two bwd_sweep launches per infcl_bwd call
+    bwd_launch_ms = sum(bwd_ms) / len(bwd_ms) / 2.0   # two sweep launches per infcl_bwd call
+    # 16-bit inputs with d = 768 or 1024 run the single-pass wide-row sweep
+    bwd_kernel = "bwd_wide" if dt_name != "f32" and d in (768, 1024) else "bwd_sweep"
     fwd_launch_ms = sum(fwd_ms) / len(fwd_ms)
     peak = FP32_MFMA_PEAK if dt_name == "f32" else BF16_PEAK  # fp16 and bf16 dense MFMA peaks are equal
     alg_bwd_launch = 3.0 * entries * d      # half of the 6 b^2 d algorithmic backward flops
@@ -200,7 +202,7 @@ def main():
     achieved = alg_bwd_launch / (bwd_launch_ms * 1e-3)
     workload = f"symmetric InfoNCE forward+backward, b={b} d={d} {dt_name}, sigma={cfg['sigma']}, s={cfg['scale']}"
     src = source_hash("bwd.hip", "bwd.hpp", "sweep.hpp", "common.hpp")
-    traffic = load_traffic("bwd_sweep", workload, src)
+    traffic = load_traffic(bwd_kernel, workload, src)
 
     out = {
         "metric": "similarity entries/s (b^2 per forward+backward pass)",
@@ -225,7 +227,7 @@ def main():
         "step_ms_min": min(step_ms),
         "peak_hbm_bytes": int(peak_bytes - base_mem + (img.numel() + txt.numel()) * img.element_size()),
         "roofline": {
-            "kernel": "bwd_sweep (one of the two backward launches)",
+            "kernel": f"{bwd_kernel} (one of the two backward launches)",
             "bound": "mfma",
             "achieved": achieved / 1e12,
             "peak": peak / 1e12,
@@ -234,8 +236,9 @@ def main():
             "traffic": traffic,
             "algorithmic_flops_per_launch": alg_bwd_launch,
             "avg_launch_ms": bwd_launch_ms,
-            "fwd_sweep": {"achieved": alg_fwd_launch / (fwd_launch_ms * 1e-3) / 1e12,
-                          "frac": alg_fwd_launch / (fwd_launch_ms * 1e-3) / peak, "avg_launch_ms": fwd_launch_ms},
+            "forward": {"kernel": "fwd_sweep2" if dt_name != "f32" and d <= 512 else "fwd_sweep",
+                        "achieved": alg_fwd_launch / (fwd_launch_ms * 1e-3) / 1e12,
+                        "frac": alg_fwd_launch / (fwd_launch_ms * 1e-3) / peak, "avg_launch_ms": fwd_launch_ms},
         },
         "cpu_baseline": None,
     }
