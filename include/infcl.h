@@ -37,6 +37,9 @@
  *     (INFCL_ERR_UNSUPPORTED otherwise).
  *   - Results are bitwise reproducible for a given (b, d, dtype): no atomics,
  *     all reductions run in a fixed order.
+ *   - The calls may be captured into a HIP graph: they enqueue kernels only
+ *     (no allocation, no memset or copy nodes, no host synchronisation), and
+ *     replays give the bits of the eager calls.
  */
 #ifndef INFCL_H
 #define INFCL_H
