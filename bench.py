@@ -36,6 +36,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=2, help="workload configuration 1..5 (default 2)")
+    ap.add_argument("--shards", type=int, default=1,
+                    help="run each step as this many shards of the batch (one GPU's share each, "
+                         "infcl_fwd_shard / _finish / infcl_bwd_shard) one after another on this device")
     ap.add_argument("--dtype", choices=["bf16", "f16", "f32"], default=None,
                     help="input type instead of the configuration's own (same shapes and scale)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -162,6 +165,29 @@ def main():
         if ev is not None:
             ev[2].record()
 
+    if a.shards > 1:
+        # the same step as a.shards shards, each a separate call; on very large
+        # batches every shard call is waited for and reported
+        from paper_2410_17243_amd import shards as shd
+
+        del ws
+        sws = [infcl.workspace_for(img) for _ in shd.shard_bounds(b, a.shards)]
+        sh_out = {"lse_r": lse_r, "lse_c": lse_c, "aux": aux, "dimg": dimg, "dtxt": dtxt}
+
+        def step(ev=None):  # noqa: F811
+            def on_step(name):
+                if ev is not None and name == "forward finished":
+                    ev[1].record()
+                if progress:
+                    torch.cuda.synchronize()
+                    note(name)
+            if ev is not None:
+                ev[0].record()
+            r = shd.sharded_forward_backward(img, txt, scale, a.shards, on_step=on_step, workspaces=sws, out=sh_out)
+            loss64.copy_(r["loss64"])
+            if ev is not None:
+                ev[2].record()
+
     note(f"inputs resident (b={b}, d={d}); first step")
     step()
     torch.cuda.synchronize()
@@ -201,6 +227,8 @@ def main():
     alg_fwd_launch = 2.0 * entries * d
     achieved = alg_bwd_launch / (bwd_launch_ms * 1e-3)
     workload = f"symmetric InfoNCE forward+backward, b={b} d={d} {dt_name}, sigma={cfg['sigma']}, s={cfg['scale']}"
+    if a.shards > 1:
+        workload += f", as {a.shards} shards"
     src = source_hash("bwd.hip", "bwd.hpp", "sweep.hpp", "common.hpp")
     traffic = load_traffic(bwd_kernel, workload, src)
 

@@ -38,25 +38,36 @@ def shard_bounds(b: int, n: int, align: int = 32):
     return bounds
 
 
-def sharded_forward_backward(img, txt, scale, n: int, dloss=None):
+def sharded_forward_backward(img, txt, scale, n: int, dloss=None, on_step=None, workspaces=None, out=None):
     """Loss, per-sample outputs and gradients of the whole batch, computed as n
     shards.  Returns a dict with loss64 (sum of the shards' shares), lse_r, lse_c,
-    aux ([3b], in infcl_fwd's layout), dimg, dtxt, dscale64 and the shard bounds."""
+    aux ([3b], in infcl_fwd's layout), dimg, dtxt, dscale64 and the shard bounds.
+
+    on_step(name), if given, is called after each shard call is enqueued (e.g.
+    to synchronise and report progress on very large batches).  workspaces (one
+    per shard) and out (a previous result) may be passed to reuse buffers."""
     import torch
 
     b, d = img.shape
     dev = img.device
     dt = _dtype_code(img)
     bounds = shard_bounds(b, n)
-    ws = [workspace_for(img) for _ in bounds]
+    ws = workspaces if workspaces is not None else [workspace_for(img) for _ in bounds]
+    note = on_step or (lambda name: None)
     # 1. local sweeps: one pair per column over each shard's rows
     colpair = [torch.empty(2 * b, dtype=torch.float32, device=dev) for _ in bounds]
-    for (r0, bs), w, cp in zip(bounds, ws, colpair):
+    for g, ((r0, bs), w, cp) in enumerate(zip(bounds, ws, colpair)):
         infcl_fwd_shard(img, txt, scale, r0, bs, cp, w)
+        note(f"forward shard {g + 1}/{len(bounds)}")
     # 2. all-to-all of column pairs, 3. finish on the column owners
-    lse_r = torch.empty(b, dtype=torch.float32, device=dev)
-    lse_c = torch.empty(b, dtype=torch.float32, device=dev)
-    aux = torch.empty(3 * b, dtype=torch.float32, device=dev)
+    if out is not None:
+        lse_r, lse_c, aux, dimg, dtxt = out["lse_r"], out["lse_c"], out["aux"], out["dimg"], out["dtxt"]
+    else:
+        lse_r = torch.empty(b, dtype=torch.float32, device=dev)
+        lse_c = torch.empty(b, dtype=torch.float32, device=dev)
+        aux = torch.empty(3 * b, dtype=torch.float32, device=dev)
+        dimg = torch.empty((b, d), dtype=torch.float32, device=dev)
+        dtxt = torch.empty((b, d), dtype=torch.float32, device=dev)
     loss_parts = torch.empty(len(bounds), dtype=torch.float64, device=dev)
     for g, ((r0, bs), w) in enumerate(zip(bounds, ws)):
         recv = torch.empty((len(bounds), 2 * bs), dtype=torch.float32, device=dev)
@@ -72,15 +83,15 @@ def sharded_forward_backward(img, txt, scale, n: int, dloss=None):
         lse_c[r0:r0 + bs] = o_lc
         for k in range(3):
             aux[k * b + r0:k * b + r0 + bs] = o_aux[k * bs:(k + 1) * bs]
+    note("forward finished")
     # 5. backward shards
-    dimg = torch.empty((b, d), dtype=torch.float32, device=dev)
-    dtxt = torch.empty((b, d), dtype=torch.float32, device=dev)
     ds_parts = torch.empty(len(bounds), dtype=torch.float64, device=dev)
     if dloss is not None:
         dloss = dloss.reshape(()).to(torch.float32).contiguous()
     for g, ((r0, bs), w) in enumerate(zip(bounds, ws)):
         infcl_bwd_shard(img, txt, scale, r0, bs, lse_r, lse_c, aux, dloss, dimg[r0:r0 + bs], dtxt[r0:r0 + bs],
                         ds_parts[g:g + 1], w)
+        note(f"backward shard {g + 1}/{len(bounds)}")
     return {
         "loss64": loss_parts.sum(), "loss_parts": loss_parts, "lse_r": lse_r, "lse_c": lse_c, "aux": aux,
         "dimg": dimg, "dtxt": dtxt, "dscale64": ds_parts.sum(), "dscale_parts": ds_parts, "bounds": bounds,
