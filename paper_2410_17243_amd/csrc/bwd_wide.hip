@@ -10,13 +10,17 @@
 // wave pair (2 ob, 2 ob + 1) holds own block ob (32 rows), each wave one half
 // of the features (d/8 VGPRs), and computes a partial S^T block over its half.
 // Per tile:
-//   GEMM1   partial S^T (32 swept x 32 own) over the wave's feature half,
-//           interleaved with the DMA of the next tile (all four waves);
+//   GEMM1   partial S^T (32 swept x 32 own) over the wave's feature half
+//           (and the DMA of the next tile's log-sum-exp slot);
 //   join    each wave hands the partner the 8 accumulator entries the
 //           partner finishes (LDS), then adds the partner's half of its own 8;
 //   G'      two exp2 per entry for the wave's 8 entries, the diagonal from
 //           expm1 terms, the dscale contribution; rounded to the input
-//           type into the shared G' block (64 own x 32 swept);
+//           type into the shared G' block (64 own x 32 swept).  The DMA of
+//           the next tile (all four waves) is issued here, between the
+//           entries: in this phase, which has no MFMAs, its instructions cost
+//           far less than between GEMM1's MFMAs (a whole-tile phase trace at
+//           d = 768: GEMM1 took 3170 cycles with the DMA and 1300 without);
 //   GEMM2   each wave multiplies all 64 own rows' G' by its quarter of the
 //           features of the tile (transposing LDS reads), accumulating in
 //           AGPRs.
@@ -34,10 +38,9 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
   constexpr int ROWG = D * 2;
   constexpr int TILEB = kBwdBN * ROWG;
   constexpr int NIW = TILEB / 4096;  // 1 KiB DMA instructions per wave and tile
-  constexpr int SPI = KH / NIW;      // GEMM1 steps per DMA instruction
   constexpr int FBW = D / 128;       // 32-feature blocks of GEMM2 per wave
   constexpr int kPre = 4;
-  static_assert(KH % 8 == 0 && KH % NIW == 0, "feature halves start on a 128-feature segment");
+  static_assert(KH % 8 == 0, "feature halves start on a 128-feature segment");
   static_assert(2 * TILEB + 2 * 1024 + kWideBM * kBwdBN * 2 + 4 * 64 * 32 + 2048 <= 160 * 1024, "LDS budget");
   __shared__ __attribute__((aligned(1024))) char tA_[TILEB];
   __shared__ __attribute__((aligned(1024))) char tB_[TILEB];
@@ -109,8 +112,8 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
     for (int r = 0; r < 16; ++r) dacc[i][r] = 0.f;
 
   // ---- GEMM1 over this wave's feature half of the tile in cur; issues the
-  // DMA of tile dtile (all four waves share it) between the MFMAs
-  auto gemm1 = [&](const INFCL_LDS char* cur, int dtile, INFCL_LDS char* ddst, INFCL_LDS float* dlse) {
+  // DMA of tile dtile's log-sum-exp slot
+  auto gemm1 = [&](const INFCL_LDS char* cur, int dtile, INFCL_LDS float* dlse) {
     int offA[8];
     {
       const int lo = opaque_lane();
@@ -120,9 +123,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
       for (int k = 0; k < 8; ++k) offA[k] = rA * kSegRow + 16 * ((2 * k + (lo >> 5)) ^ gA);
     }
     const INFCL_LDS char* half = cur + kSeg * (kh * KH / 8);
-    const u32x4 drs = tile_rsrc(dtile);
     const u32x4 drl = lse_rsrc(dtile);
-    const uint32_t dlo = sweep_dma_lane_off(opaque_lane(), wave, ROWG);
     f32x16 sacc;
     bf16x8 ring[kPre];
 #pragma unroll
@@ -131,10 +132,6 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
 #pragma unroll
     for (int s2 = 0; s2 < KH; ++s2) {
       mfma16_vgpr<F16>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KH - 1);
-      if ((s2 + 1) % SPI == 0) {
-        const int kk = (s2 + 1) / SPI - 1;
-        dma16_asm(drs, ddst + 1024 * (wave + 4 * kk), dlo + sweep_dma_kk_off(kk, wave, ROWG));
-      }
       if (s2 == 1) dma16_asm(drl, dlse, lse_lane_off());
       if (s2 + kPre < KH) {
         const int n = s2 + kPre;
@@ -146,8 +143,10 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
   };
 
   // ---- join, G' of the wave's 8 entries (entry r = 8 kh + i <-> swept row
-  // 16 kh + 8h + i of the tile) into the G' block; returns dscale's share
-  auto join_gp = [&](int jt, const INFCL_LDS float* lcur, const f32x16& sacc) -> float {
+  // 16 kh + 8h + i of the tile) into the G' block, with the DMA of tile
+  // dtile into ddst spread over the entries; returns dscale's share
+  auto join_gp = [&](int jt, const INFCL_LDS float* lcur, const f32x16& sacc, int dtile,
+                     INFCL_LDS char* ddst) -> float {
     float mine[8], other[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
@@ -166,8 +165,15 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
     const bool special = (j0 == own0) || (j0 + kBwdBN > b) || !wave_rows_ok;
     float ds_tile = 0.f;
     bf16x8 ga;
+    const u32x4 drs = tile_rsrc(dtile);
+    const uint32_t dlo = sweep_dma_lane_off(opaque_lane(), wave, ROWG);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
+#pragma unroll
+      for (int u = 0; u < (NIW + 7) / 8; ++u) {  // DMA instructions i, i + 8, ...
+        const int kk = i + 8 * u;
+        if (kk < NIW) dma16_asm(drs, ddst + 1024 * (wave + 4 * kk), dlo + sweep_dma_kk_off(kk, wave, ROWG));
+      }
       const float x = mine[i] + (i < 4 ? q0[i] : q1[i - 4]);
       const float Lj = i < 4 ? L0[i] : L1[i - 4];
       const float pO = exp2_hw(__builtin_fmaf(x, k2, -aO));
@@ -237,8 +243,9 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
   // nxt during GEMM1
   auto body = [&](int jt, const INFCL_LDS char* cur, const INFCL_LDS float* lcur, INFCL_LDS char* nxt,
                   INFCL_LDS float* lnxt) {
-    const f32x16 sacc = gemm1(cur, jt + 1 < ntile ? jt + 1 : -1, nxt, lnxt);
-    ds_acc += (double)join_gp(jt, lcur, sacc);
+    const int dtile = jt + 1 < ntile ? jt + 1 : -1;
+    const f32x16 sacc = gemm1(cur, dtile, lnxt);
+    ds_acc += (double)join_gp(jt, lcur, sacc, dtile, nxt);
     __syncthreads();  // the G' block is complete
     gemm2(cur);
     wait_dma();
