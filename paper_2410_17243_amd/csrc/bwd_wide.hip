@@ -216,11 +216,12 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
       }
     };
     // one group (contraction half s2, feature block fbw) per stage, the
-    // transposing reads one stage ahead; stages are separate scheduling
+    // transposing reads two stages ahead; stages are separate scheduling
     // regions, which keeps the read-ahead (and the registers) bounded
     bf16x8 A[2];
-    s16x4 bq[2][2];
+    s16x4 bq[3][2];
     readB(0, bq[0]);
+    readB(1, bq[1]);
 #pragma unroll
     for (int g = 0; g < 2 * FBW; ++g) {
       const int s2 = g / FBW, fbw = g % FBW;
@@ -229,8 +230,8 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
         for (int o2 = 0; o2 < 2; ++o2)
           A[o2] = *(const INFCL_LDS bf16x8*)(gp + 2048 * o2 + gpo + 16 * ((2 * s2 + ho) ^ gsw));
       }
-      if (g + 1 < 2 * FBW) readB(g + 1, bq[(g + 1) & 1]);
-      const s16x4* q = bq[g & 1];
+      if (g + 2 < 2 * FBW) readB(g + 2, bq[(g + 2) % 3]);
+      const s16x4* q = bq[g % 3];
       const s16x8 bb = {q[0][0], q[0][1], q[0][2], q[0][3], q[1][0], q[1][1], q[1][2], q[1][3]};
 #pragma unroll
       for (int o2 = 0; o2 < 2; ++o2)
