@@ -264,7 +264,7 @@ def main():
             "traffic": traffic,
             "algorithmic_flops_per_launch": alg_bwd_launch,
             "avg_launch_ms": bwd_launch_ms,
-            "forward": {"kernel": "fwd_sweep2" if dt_name != "f32" and d <= 512 else "fwd_sweep",
+            "forward": {"kernel": "fwd_sweep2" if dt_name != "f32" and d % 128 == 0 and d <= 1024 else "fwd_sweep",
                         "achieved": alg_fwd_launch / (fwd_launch_ms * 1e-3) / 1e12,
                         "frac": alg_fwd_launch / (fwd_launch_ms * 1e-3) / peak, "avg_launch_ms": fwd_launch_ms},
         },

@@ -18,7 +18,7 @@ int launch_fwd_shard_finish(int64_t b, int64_t d, int dtype, int64_t r0, int64_t
                             double* loss_part, hipStream_t stream, const float* rowR, const float* rowL,
                             const float* udiag, double* partial);
 void fwd1_grid(int64_t b, int64_t nrows, int* Pr, int* Pc);
-void fwd2_grid(int64_t b, int64_t nrows, int* Pr, int* Pc);
+void fwd2_grid(int64_t b, int64_t nrows, int64_t d, int* Pr, int* Pc);
 int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, int64_t r0, int64_t nrows,
                const float* scale, const float* lse_r, const float* lse_c, const float* aux, const float* dloss,
                float* dimg, float* dtxt, float* dscale, double* dscale64, float* lse2, double* ds_part, float* g16,
@@ -42,9 +42,12 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // as many row groups, and its row partials are nrows long.
 Layout make_layout(int64_t b) {
   Layout L;
-  int Pr = 0, Pc = 0, Pr2 = 0, Pc2 = 0;
+  int Pr = 0, Pc = 0, Pr2 = 0, Pc2 = 0, Pr3 = 0, Pc3 = 0;
   infcl::fwd1_grid(b, b, &Pr, &Pc);
-  infcl::fwd2_grid(b, b, &Pr2, &Pc2);
+  infcl::fwd2_grid(b, b, 512, &Pr2, &Pc2);
+  infcl::fwd2_grid(b, b, 1024, &Pr3, &Pc3);
+  if (Pr3 > Pr2) Pr2 = Pr3;
+  if (Pc3 > Pc2) Pc2 = Pc3;
   const size_t nrow = (size_t)(Pc * 4 > Pc2 ? Pc * 4 : Pc2), ncol = (size_t)(Pr > Pr2 ? Pr : Pr2);
   size_t off = 0;
   const size_t fb = (size_t)b * sizeof(float);

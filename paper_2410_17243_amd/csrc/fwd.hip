@@ -559,7 +559,7 @@ __global__ void __launch_bounds__(256) sum_partials(const double* part, int64_t 
 
 // ------------------------------------------------------------ host launchers
 bool fwd2_supported(int64_t d, int dtype);
-void fwd2_grid(int64_t b, int64_t nrows, int* Pr, int* Pc);
+void fwd2_grid(int64_t b, int64_t nrows, int64_t d, int* Pr, int* Pc);
 int launch_fwd2(const void* img, const void* txt, int64_t b, int64_t d, int dtype, int64_t r0, int64_t nrows,
                 const float* scale, float* rowR, float* rowL, float* colR, float* colL, float* udiag, float* ref2,
                 hipStream_t stream);
@@ -606,7 +606,7 @@ static int launch_fwd1(const void* img, const void* txt, int64_t b, int64_t d, i
 }
 
 // The sweep over own rows [r0, r0 + nrows) against all b columns: 16-bit
-// inputs with d <= 512 take the resident-rows sweep, everything else the
+// inputs with d a multiple of 128 up to 1024 take the resident-rows sweep, everything else the
 // streamed-tiles sweep above.  Both leave partial pairs: nrowpart per own row
 // (stride nrows, by row - r0) and ncolpart per column (stride b).
 static int launch_sweep(const void* img, const void* txt, int64_t b, int64_t d, int dtype, int64_t r0, int64_t nrows,
@@ -614,7 +614,7 @@ static int launch_sweep(const void* img, const void* txt, int64_t b, int64_t d, 
                         float* ref2, hipStream_t stream, int* nrowpart, int* ncolpart) {
   if (fwd2_supported(d, dtype)) {
     int Pr2 = 0, Pc2 = 0;
-    fwd2_grid(b, nrows, &Pr2, &Pc2);
+    fwd2_grid(b, nrows, d, &Pr2, &Pc2);
     *nrowpart = Pc2;
     *ncolpart = Pr2;
     return launch_fwd2(img, txt, b, d, dtype, r0, nrows, scale, rowR, rowL, colR, colL, udiag, ref2, stream);
@@ -628,7 +628,7 @@ static int launch_sweep(const void* img, const void* txt, int64_t b, int64_t d, 
 int sweep_rowparts(int64_t b, int64_t d, int dtype, int64_t nrows) {
   int Pr = 0, Pc = 0;
   if (fwd2_supported(d, dtype)) {
-    fwd2_grid(b, nrows, &Pr, &Pc);
+    fwd2_grid(b, nrows, d, &Pr, &Pc);
     return Pc;
   }
   fwd1_grid(b, nrows, &Pr, &Pc);

@@ -1,18 +1,23 @@
 // Forward sweep of the tiled symmetric InfoNCE loss with resident own rows
-// (16-bit inputs: bf16 or fp16, d <= 512, gfx950).
+// (16-bit inputs: bf16 or fp16, d a multiple of 128 up to 1024, gfx950).
 //
 // What is computed (Sec. 3.1, Eq. 2-5; the in-GPU forward of Sec. 3.2,
 // Alg. 2): the off-diagonal log-sum-exp of every row i and every column j of
 // S = s * img * txt^T, without storing S.
 //
 // Work decomposition.  Workgroup (q, g) of a P_r x P_c grid owns row blocks
-// q, q + P_r, ... of 32 NW image rows (NW = 8 waves by default; 32 rows per
-// wave, held in registers as the MFMA operand for the whole block, as Alg. 2
-// keeps its row tile on chip) and sweeps the text tiles of column group g (32
-// rows each, streamed through LDS by DMA in the swept-tile layout).  Each tile
-// is one 32 x 32 block of S^T per wave.  Only text tiles move: 32 KiB of DMA
-// per tile and workgroup for 8.4 MFLOP at d = 512 with 8 waves.  g = blockIdx mod P_c, so with P_c = 8 the workgroups
-// of a column group share one XCD and its L2.
+// q, q + P_r, ... of 32 NW image rows (32 rows per wave, held in registers as
+// the MFMA operand for the whole block, as Alg. 2 keeps its row tile on chip)
+// and sweeps the text tiles of column group g (32 rows each, streamed through
+// LDS by DMA in the swept-tile layout).  Each tile is one 32 x 32 block of S^T
+// per wave.  Only text tiles move: 32 KiB of DMA per tile and workgroup for
+// 8.4 MFLOP at d = 512 with 8 waves.  g = blockIdx mod P_c, so with P_c = 8 the
+// workgroups of a column group share one XCD and its L2.
+//  - d <= 512: NW = 8 waves, one workgroup per CU (d/4 VGPRs of own rows).
+//  - d > 512: the own rows take d/4 registers of the wave's 512, so NW = 4
+//    (one wave per SIMD) and the own-row operand lives in AGPRs, which the
+//    MFMA reads directly; this leaves the VGPRs to the tile ring and the
+//    statistics.
 //
 // Statistics.  Log-sum-exp values are kept in base 2 as running pairs (R, l)
 // meaning log2(l) + R; the empty sum is l = 0 with any finite R.  New values y
@@ -53,7 +58,7 @@ struct Fwd2Params {
   float* colR;  // [Pr][b]
   float* colL;
   int Pr, Pc;
-  int nRB;  // row blocks of kF2BM own rows
+  int nRB;  // row blocks of 32 NW own rows
   int nCT;  // column tiles of 32
 };
 
@@ -63,8 +68,31 @@ struct Fwd2Params {
 #define INFCL_FWD2_WAVES 8
 #endif
 constexpr int kF2NW = INFCL_FWD2_WAVES;
-constexpr int kF2BM = 32 * kF2NW;  // own rows per row block
+// Waves per workgroup at width d: above 512 the own rows' operand (d/4
+// registers) leaves room for one wave per SIMD only, so 4 waves (128 own
+// rows) and one workgroup per CU.
+__host__ __device__ constexpr int fwd2_waves(int64_t d) { return d > 512 ? 4 : kF2NW; }
 constexpr float kTinyBound = 5.421010862427522e-20f;  // 2^-64
+// mfma16_vgpr with the B operand (the own rows) held in AGPRs, for d > 512;
+// the same wait states around the MFMA.
+#define INFCL_MFMA16_AB(OP)                                                                                    \
+  if (first && last)                                                                                           \
+    asm volatile("s_nop 1\n\t" OP " %0, %1, %2, 0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3" : "=&v"(acc) : "v"(a), "a"(b)); \
+  else if (first)                                                                                              \
+    asm volatile("s_nop 1\n\t" OP " %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "a"(b));                              \
+  else if (last)                                                                                               \
+    asm volatile("s_nop 1\n\t" OP " %0, %1, %2, %0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3" : "+v"(acc) : "v"(a), "a"(b)); \
+  else                                                                                                         \
+    asm volatile("s_nop 1\n\t" OP " %0, %1, %2, %0" : "+v"(acc) : "v"(a), "a"(b));
+template <bool F16>
+__device__ __forceinline__ void mfma16_vgpr_ab(f32x16& acc, const bf16x8& a, const bf16x8& b, bool first, bool last) {
+  if constexpr (F16) {
+    INFCL_MFMA16_AB("v_mfma_f32_32x32x16_f16")
+  } else {
+    INFCL_MFMA16_AB("v_mfma_f32_32x32x16_bf16")
+  }
+}
+#undef INFCL_MFMA16_AB
 // Widest spread (log2 units) between the wave reference and a row or column
 // reference for which the factorised column pass keeps every entry that
 // matters: a lost term is below 2^-(126 - kWide) of its column reference.
@@ -144,15 +172,16 @@ __device__ __forceinline__ float pair_level(float R, float l) {
 }
 
 template <int D, bool F16>
-__global__ void __launch_bounds__(64 * kF2NW, 2) fwd_sweep2(Fwd2Params p) {
-  constexpr int NW = kF2NW;
+__global__ void __launch_bounds__(64 * fwd2_waves(D), D > 512 ? 1 : 2) fwd_sweep2(Fwd2Params p) {
+  constexpr int NW = fwd2_waves(D);
+  constexpr int BM = 32 * NW;  // own rows per row block
   constexpr int KS = D / 16;
   constexpr int ROWG = D * 2;
   constexpr int TILEB = kSweepBN * ROWG;
   constexpr int NIW = TILEB / 1024 / NW;  // 1 KiB DMA instructions per wave and tile
   constexpr int kPre = KS < 4 ? KS : 4;
-  static_assert(D % 64 == 0 && D <= 512 && NIW >= 1 && KS % NIW == 0, "tile DMA layout");
-  static_assert(2 * (2 * TILEB + 4 * 1024 + 5 * 512) <= 160 * 1024, "two workgroups per CU");
+  static_assert(D % 64 == 0 && D <= 1024 && NIW >= 1 && KS % NIW == 0, "tile DMA layout");
+  static_assert((D > 512 ? 1 : 2) * (2 * TILEB + 4 * 1024 + 5 * 512) <= 160 * 1024, "workgroups per CU");
   __shared__ __attribute__((aligned(1024))) char tA_[TILEB];
   __shared__ __attribute__((aligned(1024))) char tB_[TILEB];
   // running pairs of the tile's 32 columns: R at [0, 256), l at [256, 512);
@@ -211,7 +240,7 @@ __global__ void __launch_bounds__(64 * kF2NW, 2) fwd_sweep2(Fwd2Params p) {
 
   for (int rb = q; rb < p.nRB; rb += p.Pr) {
     const bool first_rb = rb == q;
-    const int own0 = p.r0 + rb * kF2BM + 32 * wave;  // r0 is a multiple of 32: own blocks stay tile-aligned
+    const int own0 = p.r0 + rb * BM + 32 * wave;  // r0 is a multiple of 32: own blocks stay tile-aligned
     const int iown = own0 + l32;
     const bool own_ok = iown < p.rend;
     const int irow = own_ok ? iown : p.rend - 1;
@@ -337,7 +366,10 @@ __global__ void __launch_bounds__(64 * kF2NW, 2) fwd_sweep2(Fwd2Params p) {
         __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
 #pragma unroll
         for (int s2 = 0; s2 < KS; ++s2) {
-          mfma16_vgpr<F16>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KS - 1);
+          if constexpr (D > 512)  // own rows in AGPRs
+            mfma16_vgpr_ab<F16>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KS - 1);
+          else
+            mfma16_vgpr<F16>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KS - 1);
           constexpr int SPI = KS / NIW;  // steps per DMA instruction
           if ((s2 + 1) % SPI == 0) {
             const int kk = kk0 + (s2 + 1) / SPI - 1;
@@ -473,22 +505,24 @@ __global__ void __launch_bounds__(64 * kF2NW, 2) fwd_sweep2(Fwd2Params p) {
 template <int D>
 static int launch_fwd2_d(const Fwd2Params& p, bool f16, hipStream_t stream) {
   if (f16)
-    hipLaunchKernelGGL((fwd_sweep2<D, true>), dim3(p.Pr * p.Pc), dim3(64 * kF2NW), 0, stream, p);
+    hipLaunchKernelGGL((fwd_sweep2<D, true>), dim3(p.Pr * p.Pc), dim3(64 * fwd2_waves(D)), 0, stream, p);
   else
-    hipLaunchKernelGGL((fwd_sweep2<D, false>), dim3(p.Pr * p.Pc), dim3(64 * kF2NW), 0, stream, p);
+    hipLaunchKernelGGL((fwd_sweep2<D, false>), dim3(p.Pr * p.Pc), dim3(64 * fwd2_waves(D)), 0, stream, p);
   return hipGetLastError() == hipSuccess ? 0 : 1;
 }
 
-// 16-bit inputs (bf16 = 0, fp16 = 2) with d <= 512
-bool fwd2_supported(int64_t d, int dtype) {
-  return (dtype == 0 || dtype == 2) && (d == 128 || d == 256 || d == 384 || d == 512);
-}
+// 16-bit inputs (bf16 = 0, fp16 = 2) with d a multiple of 128 up to 1024
+bool fwd2_supported(int64_t d, int dtype) { return (dtype == 0 || dtype == 2) && d % 128 == 0 && d >= 128 && d <= 1024; }
 
-// Grid of the resident-rows forward for nrows own rows against b columns.
-void fwd2_grid(int64_t b, int64_t nrows, int* Pr, int* Pc) {
-  const int64_t nRB = (nrows + kF2BM - 1) / kF2BM, nCT = (b + kSweepBN - 1) / kSweepBN;
+// Grid of the resident-rows forward for nrows own rows of width d against b
+// columns: P_c column groups (one per XCD) times P_r row groups, P_r P_c <= 256
+// workgroups (one per CU) with 8 waves or with 4 waves at d > 512, and 512 (two
+// per CU) with the 4-wave build option at d <= 512.
+void fwd2_grid(int64_t b, int64_t nrows, int64_t d, int* Pr, int* Pc) {
+  const int64_t bm = 32 * fwd2_waves(d);
+  const int64_t nRB = (nrows + bm - 1) / bm, nCT = (b + kSweepBN - 1) / kSweepBN;
   *Pc = (int)(nCT < 8 ? nCT : 8);
-  const int64_t pmax = 256 / kF2NW;  // P_r P_c <= 2048 / NW: two workgroups per CU with 4 waves, one with 8
+  const int64_t pmax = d > 512 ? 32 : 256 / kF2NW;
   *Pr = (int)(nRB < pmax ? nRB : pmax);
 }
 
@@ -516,14 +550,18 @@ int launch_fwd2(const void* img, const void* txt, int64_t b, int64_t d, int dtyp
   p.r0 = (int)r0;
   p.rend = (int)(r0 + nrows);
   p.rstride = nrows;
-  fwd2_grid(b, nrows, &p.Pr, &p.Pc);
-  p.nRB = (int)((nrows + kF2BM - 1) / kF2BM);
+  fwd2_grid(b, nrows, d, &p.Pr, &p.Pc);
+  p.nRB = (int)((nrows + 32 * fwd2_waves(d) - 1) / (32 * fwd2_waves(d)));
   p.nCT = (int)((b + kSweepBN - 1) / kSweepBN);
   switch (d) {
     case 128: return launch_fwd2_d<128>(p, f16, stream);
     case 256: return launch_fwd2_d<256>(p, f16, stream);
     case 384: return launch_fwd2_d<384>(p, f16, stream);
     case 512: return launch_fwd2_d<512>(p, f16, stream);
+    case 640: return launch_fwd2_d<640>(p, f16, stream);
+    case 768: return launch_fwd2_d<768>(p, f16, stream);
+    case 896: return launch_fwd2_d<896>(p, f16, stream);
+    case 1024: return launch_fwd2_d<1024>(p, f16, stream);
   }
   return 2;
 }
