@@ -71,6 +71,45 @@ def load_traffic(kernel: str, workload: str, src: str):
         return None
 
 
+def smi_reading(text: str):
+    """(sclk MHz, junction or edge temperature in C) from `rocm-smi --json`
+    output; None for what it does not hold."""
+    import re
+    try:
+        cards = json.loads(text)
+    except ValueError:
+        return None, None
+    card = next(iter(cards.values()), {}) if isinstance(cards, dict) and cards else {}
+    sclk = temp = None
+    for k, v in card.items() if isinstance(card, dict) else []:
+        kl = k.lower()
+        m = re.search(r"(\d+(?:\.\d+)?)", str(v))
+        if not m:
+            continue
+        if "sclk" in kl and sclk is None:
+            sclk = float(m.group(1))
+        elif "temperature" in kl and ("junction" in kl or ("edge" in kl and temp is None)):
+            temp = float(m.group(1))
+    return sclk, temp
+
+
+def device_info(torch):
+    """Name, architecture and CU count of device 0, and its shader clock and
+    temperature as rocm-smi reads them right after the timed steps (None
+    where the tool is missing or prints something else)."""
+    import subprocess
+    pr = torch.cuda.get_device_properties(0)
+    info = {"name": pr.name, "arch": getattr(pr, "gcnArchName", None), "cus": pr.multi_processor_count,
+            "sclk_mhz_after": None, "temp_c_after": None}
+    try:
+        r = subprocess.run(["rocm-smi", "-d", "0", "--showclocks", "--showtemp", "--json"], capture_output=True,
+                           text=True, timeout=20)
+        info["sclk_mhz_after"], info["temp_c_after"] = smi_reading(r.stdout)
+    except (OSError, subprocess.SubprocessError):
+        pass
+    return info
+
+
 def cpu_baseline(cfg, sample_b):
     """The fp64 oracle (as it stands) on a bounded sample of the same workload."""
     import oracle
@@ -97,8 +136,9 @@ def cpu_baseline(cfg, sample_b):
 def main():
     a = parse()
     if a.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {a.gpus}); this build has no multi-GPU path.",
-              file=sys.stderr)
+        print(f"bench.py measures one GPU only (got --gpus {a.gpus}): the library has no collective path. "
+              "Its shard entry points compute one GPU's share of a batch sharded over n GPUs; "
+              "--shards n times all n shares one after another on this device.", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
@@ -115,7 +155,7 @@ def main():
     import paper_2410_17243_amd as infcl
     from paper_2410_17243_amd import synth
 
-    cfg = dict(synth.CONFIGS[a.config])
+    cfg = dict(synth.WORKLOADS[a.config])
     if a.dtype is not None:
         cfg["dtype"] = a.dtype
     b, d, dt_name = cfg["b"], cfg["d"], cfg["dtype"]
@@ -269,6 +309,7 @@ def main():
                         "frac": alg_fwd_launch / (fwd_launch_ms * 1e-3) / peak, "avg_launch_ms": fwd_launch_ms},
         },
         "cpu_baseline": None,
+        "device": device_info(torch),
     }
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, min(a.cpu_sample_b, b))

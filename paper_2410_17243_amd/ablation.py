@@ -31,7 +31,7 @@ def main(argv=None):
     import paper_2410_17243_amd as infcl
     from paper_2410_17243_amd import synth
 
-    cfg = synth.CONFIGS[a.config]
+    cfg = synth.WORKLOADS[a.config]
     b, d = cfg["b"], cfg["d"]
     dev = torch.device("cuda:0")
     img_np, txt_np = synth.clip_pairs(b, d, cfg["sigma"], seed=0, dtype=cfg["dtype"])

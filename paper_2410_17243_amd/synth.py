@@ -88,7 +88,7 @@ def as_f64(a: np.ndarray, dtype: str) -> np.ndarray:
 
 
 # The five workloads: shapes, noise and scale of the benchmark configurations.
-CONFIGS = {
+WORKLOADS = {
     1: dict(b=1024, d=512, dtype="f32", sigma=1.0, scale=1.0 / 0.07),
     2: dict(b=32768, d=512, dtype="bf16", sigma=1.0, scale=14.29),
     3: dict(b=131072, d=768, dtype="bf16", sigma=0.5, scale=100.0),

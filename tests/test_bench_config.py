@@ -34,7 +34,7 @@ def _grad_rows(A, B, s, rows, lse_own_rows, lse_other_all, ell_own_rows, ell_oth
 
 @pytest.mark.parametrize("cfg", [2, 3, 4])
 def test_full_size_sampled(cfg):
-    c = synth.CONFIGS[cfg]
+    c = synth.WORKLOADS[cfg]
     b, d, s = c["b"], c["d"], f32_scale(c["scale"])
     img, txt = synth.clip_pairs(b, d, c["sigma"], seed=0, dtype="bf16")
     g = run(img, txt, "bf16", s)

@@ -137,7 +137,7 @@ def test_fp32_inputs(b, d):
 
 def test_config1_fp32_workload():
     """b=1024, d=512, fp32, sigma=1, s=1/0.07, seed 0: the whole small workload."""
-    c = synth.CONFIGS[1]
+    c = synth.WORKLOADS[1]
     gpu, fwd, dI, dT, ds, s = _case(c["b"], c["d"], c["scale"], sigma=c["sigma"], dtype="f32", seed=0)
     _check(gpu, fwd, dI, dT, ds, s, c["d"], "f32")
 

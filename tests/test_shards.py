@@ -85,7 +85,7 @@ def test_sharded_full_size_workload_2():
     """b = 32768, d = 512 (the benchmark shapes) as 8 shards of 4096 samples,
     the share of each of 8 GPUs: against the whole-batch result and the
     invariant <dI, I> = <dT, T> = s * dscale."""
-    cfg = synth.CONFIGS[2]
+    cfg = synth.WORKLOADS[2]
     b, d = cfg["b"], cfg["d"]
     img, txt = synth.clip_pairs(b, d, cfg["sigma"], seed=0, dtype="bf16")
     s = f32_scale(cfg["scale"])
