@@ -191,7 +191,8 @@ const char* infcl_status_str(int status) {
   switch (status) {
     case INFCL_OK: return "ok";
     case INFCL_ERR_INVALID: return "invalid argument (null or misaligned pointer, b < 1, d < 1 or unknown dtype)";
-    case INFCL_ERR_UNSUPPORTED: return "unsupported shape (bf16: d in 128..1024 step 128; f32: d in 64..512 step 64)";
+    case INFCL_ERR_UNSUPPORTED:
+      return "unsupported shape (bf16, f16: d in 128..1024 step 128; f32: d in 64..512 step 64; b <= 2^30)";
     case INFCL_ERR_WORKSPACE: return "workspace smaller than infcl_workspace_size()";
     case INFCL_ERR_HIP: return "HIP kernel launch failed";
     default: return "unknown status";
