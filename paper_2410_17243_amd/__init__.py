@@ -172,12 +172,30 @@ def _validate(img, txt, scale):
 
     if not (img.is_cuda and txt.is_cuda and scale.is_cuda):
         raise ValueError("img, txt and scale must be device tensors")
+    if not (img.device == txt.device == scale.device):
+        raise ValueError(f"img, txt and scale must be on one device, got {img.device}, {txt.device}, {scale.device}")
     if img.shape != txt.shape or img.dim() != 2 or img.dtype != txt.dtype:
         raise ValueError(f"img and txt must be [b, d] of one dtype, got {tuple(img.shape)}, {tuple(txt.shape)}")
     if not (img.is_contiguous() and txt.is_contiguous()):
         raise ValueError("img and txt must be contiguous")
     if scale.numel() != 1 or scale.dtype != torch.float32:
         raise ValueError("scale must be a float32 tensor with one element")
+
+
+def _check_vec(t, n: int, name: str, dev):
+    """t must be a contiguous float32 device tensor of n elements on dev."""
+    import torch
+
+    if t.device != dev or t.dtype != torch.float32 or t.numel() != n or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous float32 tensor of {n} elements on {dev}, "
+                         f"got {t.dtype} {tuple(t.shape)} on {t.device}")
+
+
+def _check_workspace(ws, dev):
+    import torch
+
+    if ws.device != dev or ws.dtype != torch.uint8 or not ws.is_contiguous():
+        raise ValueError(f"workspace must be a contiguous uint8 tensor on {dev}, got {ws.dtype} on {ws.device}")
 
 
 def workspace_for(img):
@@ -202,6 +220,7 @@ def clip_loss_fwd(img, txt, scale, workspace=None) -> dict:
         "aux": torch.empty(3 * b, dtype=torch.float32, device=dev),
     }
     ws = workspace if workspace is not None else workspace_for(img)
+    _check_workspace(ws, dev)
     infcl_fwd(img, txt, scale.reshape(()), out["loss"], out["loss64"], out["lse_r"], out["lse_c"], out["aux"], ws)
     out["workspace"] = ws
     return out
@@ -210,14 +229,22 @@ def clip_loss_fwd(img, txt, scale, workspace=None) -> dict:
 def clip_loss_bwd(img, txt, scale, fwd: dict, dloss=None, workspace=None):
     import torch
 
+    _validate(img, txt, scale)
     b, d = img.shape
+    dev = img.device
+    _check_vec(fwd["lse_r"], b, "lse_r", dev)
+    _check_vec(fwd["lse_c"], b, "lse_c", dev)
+    _check_vec(fwd["aux"], 3 * b, "aux", dev)
     dimg = torch.empty((b, d), dtype=torch.float32, device=img.device)
     dtxt = torch.empty((b, d), dtype=torch.float32, device=img.device)
     dscale = torch.empty((), dtype=torch.float32, device=img.device)
     ws = workspace if workspace is not None else fwd.get("workspace")
     if ws is None:
         ws = workspace_for(img)
+    _check_workspace(ws, dev)
     if dloss is not None:
+        if dloss.device != dev or dloss.numel() != 1:
+            raise ValueError(f"dloss must be one element on {dev}, got {tuple(dloss.shape)} on {dloss.device}")
         dloss = dloss.reshape(()).to(torch.float32).contiguous()
     infcl_bwd(img, txt, scale.reshape(()), fwd["lse_r"], fwd["lse_c"], fwd["aux"], dloss, dimg, dtxt, dscale, ws)
     return dimg, dtxt, dscale
