@@ -121,7 +121,6 @@ def _device_onehot(b, d):
 def _check_C_on_device(b, d, s32, f, grads=None):
     """Closed form C checked on the device, rows in chunks (the full-size
     matrices stay on the GPU; only maxima come back)."""
-    cls_np = np.arange(d)
     n = np.bincount(np.arange(b) % d, minlength=d).astype(np.float64)
     es = math.exp(s32)
     Zc = n * es + (b - n)
@@ -138,11 +137,22 @@ def _check_C_on_device(b, d, s32, f, grads=None):
     dI, dT, dscale = grads
     ds_ref = -(1.0 / b) * math.fsum(n * (b - n) / Zc)
     assert abs(dscale - ds_ref) <= 2e-2 * abs(ds_ref) + 2.0 ** -120
+    worst = max(_check_C_grad_rows(b, d, s32, g, 0) for g in (dI, dT))
+    print(f"  closed form C at b={b}: gradient error / bound {worst:.2e}", flush=True)
+    assert worst <= 1.0
+
+
+def _check_C_grad_rows(b, d, s32, g, r0):
+    """Largest |g - closed form C| / bound over the rows of g, which hold the
+    gradients of samples r0, r0 + 1, ... (class (r0 + i) mod d)."""
+    n = np.bincount(np.arange(b) % d, minlength=d).astype(np.float64)
+    es = math.exp(s32)
+    Zc = n * es + (b - n)
     # per class c: expected row coef[c] and bound[c] (see _closed_C)
     coef = np.zeros((d, d))
     absg = np.zeros((d, d))
     ell = np.log(n + (b - n) * math.exp(-s32))
-    for c in cls_np:
+    for c in range(d):
         row = n * (1.0 / Zc[c] + 1.0 / Zc) / (2 * b)
         row[c] = -(b - n[c]) / (b * Zc[c])
         coef[c] = s32 * row
@@ -153,22 +163,19 @@ def _check_C_on_device(b, d, s32, f, grads=None):
     coef_t = torch.tensor(coef, dtype=torch.float64, device="cuda")
     slack = torch.tensor(bound + 1e-3 * np.max(np.abs(coef)), dtype=torch.float64, device="cuda")
     worst = 0.0
-    for g in (dI, dT):
-        for r0 in range(0, b, 65536):
-            r1 = min(b, r0 + 65536)
-            c = torch.arange(r0, r1, device="cuda") % d
-            e = ((g[r0:r1].double() - coef_t[c]).abs() / slack[c]).max().item()
-            worst = max(worst, e)
-    print(f"  closed form C at b={b}: gradient error / bound {worst:.2e}", flush=True)
-    assert worst <= 1.0
+    for c0 in range(0, g.shape[0], 65536):
+        c1 = min(g.shape[0], c0 + 65536)
+        c = (torch.arange(c0, c1, device="cuda") + r0) % d
+        worst = max(worst, ((g[c0:c1].double() - coef_t[c]).abs() / slack[c]).max().item())
+    return worst
 
 
 @pytest.mark.parametrize("b,d,s,with_bwd", [(1048576, 1024, 50.0, True), (4194304, 768, 14.29, False)])
 def test_C_periodic_full_size(b, d, s, with_bwd):
     """Closed form C at the two largest workloads, inputs built on the device:
-    b = 1M, d = 1024, s = 50 forward and backward; b = 4M, d = 768 forward (its
-    backward takes minutes; the same backward code runs at b = 131072, d = 768
-    above and in the sampled full-size test)."""
+    b = 1M, d = 1024, s = 50 forward and backward; b = 4M, d = 768 forward and
+    the backward of two ranges of own samples (the whole backward takes
+    minutes; every own row sweeps all 4M swept rows either way)."""
     import paper_2410_17243_amd as infcl
 
     s32 = f32_scale(s)
@@ -185,3 +192,24 @@ def test_C_periodic_full_size(b, d, s, with_bwd):
         torch.cuda.synchronize()
         grads = (dI, dT, float(dscale.item()))
     _check_C_on_device(b, d, s32, f, grads)
+    if not with_bwd:
+        # the backward for two ranges of own samples against all b swept
+        # samples (the shard entry point; same kernels and 64-bit offsets as
+        # the whole-batch backward): the last 65536 samples, and a ragged
+        # range in the middle; dscale_part is the range's share of dL/ds
+        n = np.bincount(np.arange(b) % d, minlength=d).astype(np.float64)
+        Zc = n * math.exp(s32) + (b - n)
+        for r0, bs in ((b - 65536, 65536), (b // 2 + 32 * 7, 65523)):
+            print(f"  backward of samples [{r0}, {r0 + bs})", flush=True)
+            dI = torch.empty((bs, d), dtype=torch.float32, device="cuda")
+            dT = torch.empty((bs, d), dtype=torch.float32, device="cuda")
+            dsp = torch.empty(1, dtype=torch.float64, device="cuda")
+            infcl.infcl_bwd_shard(I, T, sc, r0, bs, f["lse_r"], f["lse_c"], f["aux"], None, dI, dT, dsp,
+                                  f["workspace"])
+            torch.cuda.synchronize()
+            worst = max(_check_C_grad_rows(b, d, s32, g, r0) for g in (dI, dT))
+            cls = np.arange(r0, r0 + bs) % d
+            ds_ref = -(1.0 / b) * math.fsum((b - n[cls]) / Zc[cls])
+            print(f"    gradient error / bound {worst:.2e}; dscale part {dsp.item():.6e} vs {ds_ref:.6e}", flush=True)
+            assert worst <= 1.0
+            assert abs(dsp.item() - ds_ref) <= 2e-2 * abs(ds_ref)
