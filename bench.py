@@ -164,10 +164,11 @@ def main():
 
     # the large workloads take seconds to minutes per step: say so on stderr
     progress = b >= (1 << 17)
+    t_start = time.perf_counter()
 
     def note(msg):
-        if progress:
-            print(f"[bench config {a.config}] {msg}", file=sys.stderr, flush=True)
+        if progress:  # with the seconds since start: per-shard times and their trend under sustained load
+            print(f"[bench config {a.config} +{time.perf_counter() - t_start:.1f} s] {msg}", file=sys.stderr, flush=True)
 
     note("generating inputs on the host")
     img_np, txt_np = synth.clip_pairs(b, d, cfg["sigma"], seed=0, dtype=dt_name)

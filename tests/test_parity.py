@@ -76,11 +76,13 @@ def _case_bits(img, txt, s):
     return run(img, txt, "bf16", s32), fwd, dI, dT, ds, s32
 
 
-def test_sign_flipped_pairs_bf16():
+@pytest.mark.parametrize("d", [256, 768])
+def test_sign_flipped_pairs_bf16(d):
     """txt_i = -img_i for a third of the pairs (in runs of 37), s = 100: the
     diagonal values sit at +-144 in base-2 units, so row and column references
-    lie far apart and far above most entries."""
-    b, d = 1500, 256
+    lie far apart and far above most entries (d = 768: the 4-wave forward and
+    the wide backward)."""
+    b = 1500
     img, _ = synth.clip_pairs(b, d, 0.3, seed=21, dtype="bf16")
     txt = img.copy()
     flip = (np.arange(b) // 37) % 3 == 0
@@ -89,10 +91,11 @@ def test_sign_flipped_pairs_bf16():
     _check(gpu, fwd, dI, dT, ds, s, d, "bf16")
 
 
-def test_mixed_row_norms_bf16():
+@pytest.mark.parametrize("d", [384, 896])
+def test_mixed_row_norms_bf16(d):
     """Rows scaled by 2^-2 .. 2^2 (exact in bf16): entries of one tile spread
     over a range several times that of unit rows."""
-    b, d = 1300, 384
+    b = 1300
     img, txt = synth.clip_pairs(b, d, 1.0, seed=23, dtype="bf16")
     fi = synth.as_f64(img, "bf16") * (2.0 ** ((np.arange(b) % 5) - 2))[:, None]
     ft = synth.as_f64(txt, "bf16") * (2.0 ** ((np.arange(b) * 3 % 5) - 2))[:, None]
@@ -117,8 +120,8 @@ def test_dloss_scaling_bf16():
 @pytest.mark.parametrize("b,d", [(1, 128), (65, 128), (1025, 256), (777, 512), (777, 640), (700, 768), (600, 1024)])
 def test_fp16_inputs(b, d):
     """IEEE half embeddings (the paper's mixed-precision training type): the
-    resident-rows forward (d <= 512), the streamed forward (d > 512), the
-    128-row backward and the wide backward (d = 768, 1024)."""
+    resident-rows forward (8 waves at d <= 512, 4 above), the 128-row backward
+    and the wide backward (d = 768, 1024)."""
     gpu, fwd, dI, dT, ds, s = _case(b, d, 14.29, dtype="f16", seed=b + d)
     _check(gpu, fwd, dI, dT, ds, s, d, "f16")
 
