@@ -292,6 +292,8 @@ def main():
         "mfma_frac_executed": 10.0 * entries * d / (ms_per_step * 1e-3) / peak,
         "fwd_ms": fwd_launch_ms,
         "bwd_ms": 2.0 * bwd_launch_ms,
+        "fwd_entries_per_s": entries / (fwd_launch_ms * 1e-3),
+        "bwd_entries_per_s": entries / (2.0 * bwd_launch_ms * 1e-3),
         "ms_per_step_host_wall": ms_wall,
         "step_ms_min": min(step_ms),
         "peak_hbm_bytes": int(peak_bytes - base_mem + (img.numel() + txt.numel()) * img.element_size()),
