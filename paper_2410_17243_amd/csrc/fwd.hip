@@ -472,15 +472,31 @@ struct FinParams {
   double* partial;     // [gridDim.x]
 };
 
-// natural-log log-sum-exp of n base-2 partial pairs (R, l) at R/L[k stride + t]
+// natural-log log-sum-exp of n base-2 partial pairs (R, l) at R/L[k stride + t].
+// Both passes keep eight loads in flight (one load per iteration, each waited
+// for, made the merge latency-bound); an empty pair (R = -inf) is weighted by
+// zero.  The sum runs in the same order as a plain loop over k.
 __device__ __forceinline__ double merge_parts(const float* R, const float* L, int n, int64_t stride, int64_t t) {
   double M = -__builtin_inf();
+#pragma unroll 8
   for (int k = 0; k < n; ++k) M = fmax(M, (double)R[(int64_t)k * stride + t]);
   if (M == -__builtin_inf()) return -__builtin_inf();
   double S = 0.0;
-  for (int k = 0; k < n; ++k) {
-    double r = R[(int64_t)k * stride + t];
-    if (r != -__builtin_inf()) S += (double)L[(int64_t)k * stride + t] * exp2(r - M);
+  int k = 0;
+  for (; k + 8 <= n; k += 8) {  // the eight pairs' loads first, then their terms
+    float r[8], l[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      r[u] = R[(int64_t)(k + u) * stride + t];
+      l[u] = L[(int64_t)(k + u) * stride + t];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) S += r[u] != -__builtin_inff() ? (double)l[u] * exp2((double)r[u] - M) : 0.0;
+  }
+  for (; k < n; ++k) {
+    const double r = R[(int64_t)k * stride + t];
+    const double l = L[(int64_t)k * stride + t];
+    S += r != -__builtin_inf() ? l * exp2(r - M) : 0.0;
   }
   return (M + log2(S)) * 0.6931471805599453;  // natural-log LSE over the off-diagonal entries
 }
