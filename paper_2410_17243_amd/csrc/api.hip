@@ -19,6 +19,7 @@ int launch_fwd_shard_finish(int64_t b, int64_t d, int dtype, int64_t r0, int64_t
                             const float* udiag, double* partial);
 void fwd1_grid(int64_t b, int64_t nrows, int* Pr, int* Pc);
 void fwd2_grid(int64_t b, int64_t nrows, int64_t d, int* Pr, int* Pc);
+bool fwd2_supported(int64_t d, int dtype);
 int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, int64_t r0, int64_t nrows,
                const float* scale, const float* lse_r, const float* lse_c, const float* aux, const float* dloss,
                float* dimg, float* dtxt, float* dscale, double* dscale64, float* lse2, double* ds_part, float* g16,
@@ -36,19 +37,26 @@ struct Layout {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Partial-pair regions sized for either forward sweep over all b rows
-// (streamed tiles: 4 Pc row partials, Pr column partials; resident rows: Pc2
-// and Pr2).  A shard of nrows <= b rows needs no more: its grids have at most
-// as many row groups, and its row partials are nrows long.
-Layout make_layout(int64_t b) {
+// Workspace regions, sized for the sweeps that (b, d, dtype) launches: the
+// partial pairs of the forward grid (resident rows: Pc row and Pr column
+// partials per sample; streamed tiles: 4 Pc and Pr), the diagonal, the base-2
+// diagonal references (resident rows only), the loss and dscale partials, the
+// base-2 log-sum-exp vectors of the backward and fp16's G' scale.  A shard of
+// nrows <= b rows needs no more: its grid has at most as many row groups and
+// its row partials are nrows long.
+Layout make_layout(int64_t b, int64_t d, int dtype) {
   Layout L;
-  int Pr = 0, Pc = 0, Pr2 = 0, Pc2 = 0, Pr3 = 0, Pc3 = 0;
-  infcl::fwd1_grid(b, b, &Pr, &Pc);
-  infcl::fwd2_grid(b, b, 512, &Pr2, &Pc2);
-  infcl::fwd2_grid(b, b, 1024, &Pr3, &Pc3);
-  if (Pr3 > Pr2) Pr2 = Pr3;
-  if (Pc3 > Pc2) Pc2 = Pc3;
-  const size_t nrow = (size_t)(Pc * 4 > Pc2 ? Pc * 4 : Pc2), ncol = (size_t)(Pr > Pr2 ? Pr : Pr2);
+  int Pr = 0, Pc = 0;
+  size_t nrow = 0, ncol = 0;
+  const bool resident = infcl::fwd2_supported(d, dtype);
+  if (resident) {
+    infcl::fwd2_grid(b, b, d, &Pr, &Pc);
+    nrow = (size_t)Pc;
+  } else {
+    infcl::fwd1_grid(b, b, &Pr, &Pc);
+    nrow = (size_t)Pc * 4;
+  }
+  ncol = (size_t)Pr;
   size_t off = 0;
   const size_t fb = (size_t)b * sizeof(float);
   L.rowR = off; off = align256(off + nrow * fb);
@@ -56,11 +64,11 @@ Layout make_layout(int64_t b) {
   L.colR = off; off = align256(off + ncol * fb);
   L.colL = off; off = align256(off + ncol * fb);
   L.udiag = off; off = align256(off + fb);
-  L.ref2 = off; off = align256(off + fb);
+  L.ref2 = off; off = align256(off + (resident ? fb : 0));
   L.fwd_part = off; off = align256(off + (size_t)((b + 255) / 256) * sizeof(double));
   L.lse2 = off; off = align256(off + 2 * fb);
   L.bwd_part = off; off = align256(off + (size_t)2 * ((b + 63) / 64) * sizeof(double));  // 64 or 128 rows per WG
-  L.g16 = off; off = align256(off + (size_t)(2 + 2 * ((b + 255) / 256)) * sizeof(float));  // fp16 G' scale
+  L.g16 = off; off = align256(off + (dtype == INFCL_F16 ? (size_t)(2 + 2 * ((b + 255) / 256)) * sizeof(float) : 0));
   L.total = off;
   return L;
 }
@@ -86,7 +94,7 @@ extern "C" {
 infcl_status infcl_workspace_size(int64_t b, int64_t d, int dtype, size_t* bytes) {
   if (bytes == nullptr || !shape_ok(b, d, dtype)) return INFCL_ERR_INVALID;
   if (!shape_supported(b, d, dtype)) return INFCL_ERR_UNSUPPORTED;
-  *bytes = make_layout(b).total;
+  *bytes = make_layout(b, d, dtype).total;
   return INFCL_OK;
 }
 
@@ -99,7 +107,7 @@ infcl_status infcl_fwd(const void* img, const void* txt, int64_t b, int64_t d, i
     return INFCL_ERR_INVALID;
   if (loss64 != nullptr && ((uintptr_t)loss64 % 8) != 0) return INFCL_ERR_INVALID;
   if (!shape_supported(b, d, dtype)) return INFCL_ERR_UNSUPPORTED;
-  const Layout L = make_layout(b);
+  const Layout L = make_layout(b, d, dtype);
   if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)workspace;
   int rc = infcl::launch_fwd(img, txt, b, d, dtype, scale, loss, loss64, lse_r, lse_c, aux, (hipStream_t)stream,
@@ -119,7 +127,7 @@ infcl_status infcl_bwd(const void* img, const void* txt, int64_t b, int64_t d, i
     return INFCL_ERR_INVALID;
   if (dloss != nullptr && ((uintptr_t)dloss % 4) != 0) return INFCL_ERR_INVALID;
   if (!shape_supported(b, d, dtype)) return INFCL_ERR_UNSUPPORTED;
-  const Layout L = make_layout(b);
+  const Layout L = make_layout(b, d, dtype);
   if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)workspace;
   int rc = infcl::launch_bwd(img, txt, b, d, dtype, 0, b, scale, lse_r, lse_c, aux, dloss, dimg, dtxt, dscale, nullptr,
@@ -139,7 +147,7 @@ infcl_status infcl_fwd_shard(const void* img, const void* txt, int64_t b, int64_
       !aligned(workspace, 256))
     return INFCL_ERR_INVALID;
   if (!shape_supported(b, d, dtype)) return INFCL_ERR_UNSUPPORTED;
-  const Layout L = make_layout(b);
+  const Layout L = make_layout(b, d, dtype);
   if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)workspace;
   int rc = infcl::launch_fwd_shard(img, txt, b, d, dtype, r0, bs, scale, colpair, (hipStream_t)stream,
@@ -156,7 +164,7 @@ infcl_status infcl_fwd_shard_finish(int64_t b, int64_t d, int dtype, int64_t r0,
       !aligned(loss_part, 8) || !aligned(workspace, 256))
     return INFCL_ERR_INVALID;
   if (!shape_supported(b, d, dtype)) return INFCL_ERR_UNSUPPORTED;
-  const Layout L = make_layout(b);
+  const Layout L = make_layout(b, d, dtype);
   if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)workspace;
   int rc = infcl::launch_fwd_shard_finish(b, d, dtype, r0, bs, nparts, colpairs, scale, lse_r, lse_c, aux, loss_part,
@@ -177,7 +185,7 @@ infcl_status infcl_bwd_shard(const void* img, const void* txt, int64_t b, int64_
     return INFCL_ERR_INVALID;
   if (dloss != nullptr && ((uintptr_t)dloss % 4) != 0) return INFCL_ERR_INVALID;
   if (!shape_supported(b, d, dtype)) return INFCL_ERR_UNSUPPORTED;
-  const Layout L = make_layout(b);
+  const Layout L = make_layout(b, d, dtype);
   if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)workspace;
   int rc = infcl::launch_bwd(img, txt, b, d, dtype, r0, bs, scale, lse_r, lse_c, aux, dloss, dimg, dtxt, nullptr,

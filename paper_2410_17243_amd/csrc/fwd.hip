@@ -1,4 +1,6 @@
-// Forward sweep of the tiled symmetric InfoNCE loss (gfx950).
+// Forward sweep of the tiled symmetric InfoNCE loss for fp32 inputs (gfx950),
+// and the finalize shared by both forward sweeps.  (16-bit inputs take the
+// resident-rows sweep of fwd2.hip.)
 //
 // What is computed (paper Sec. 3.1, Eq. 2-5; the in-GPU forward algorithm of
 // Sec. 3.2): for every row i and column j of S = s * img * txt^T, the
@@ -27,8 +29,6 @@
 // not finite, e.g. while R is still -inf) is redone with the exact max-rescaled
 // merge.  The paper's merge starts from 0; the identity of the merge is the
 // empty sum (R = -inf, l = 0), which is what is used here.
-#include <type_traits>
-
 #include "common.hpp"
 
 namespace infcl {
@@ -79,10 +79,9 @@ __device__ __forceinline__ FwdDmaOffsets fwd_dma_offsets(int64_t d, int es, int 
 
 // Issue the DMA of one K-stage (128 bytes of each of the 320 tile rows).  Rows
 // past b fall outside the buffer resources and load as zeros (they are masked).
-template <typename TIN>
 __device__ __forceinline__ void fwd_stage_dma(const FwdParams& p, const FwdDmaOffsets& o, int64_t i0, int64_t j0,
                                               int st, INFCL_LDS char* buf, int wave) {
-  const int64_t b = p.b, rowb = p.d * (int64_t)sizeof(TIN);
+  const int64_t b = p.b, rowb = p.d * (int64_t)sizeof(float);
   const u32x4 ri = rsrc_words((const char*)p.img + i0 * rowb, (p.rend - i0) * rowb);
   const u32x4 rt = rsrc_words((const char*)p.txt + j0 * rowb, (b - j0) * rowb);
   const uint32_t soff = (uint32_t)st * 128u;
@@ -92,58 +91,33 @@ __device__ __forceinline__ void fwd_stage_dma(const FwdParams& p, const FwdDmaOf
 }
 
 // MFMA work of one K-stage: acc[mb][nb] += S^T block (j block mb, i block nb).
-template <typename TIN>
-__device__ __forceinline__ void fwd_stage_mfma(const INFCL_LDS char* buf, f32x16 (&acc)[2][2], int wave,
-                                               int lane) {
+// A 16-wide fp32 contraction step is 64 bytes; lane half h holds floats 8h..8h+7.
+__device__ __forceinline__ void fwd_stage_mfma(const INFCL_LDS char* buf, f32x16 (&acc)[2][2], int wave, int lane) {
   const int l32 = lane & 31, h = lane >> 5;
-  if constexpr (sizeof(TIN) == 2) {
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int c = 2 * s + h;
-      bf16x8 a[2], bb[2];
+  for (int s = 0; s < 2; ++s) {
+    f32x4 a[2][2], bb[2][2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int c = 4 * s + 2 * h + u;
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb) {
         int r = kFwdBI + 64 * wave + 32 * mb + l32;
-        a[mb] = *(const INFCL_LDS bf16x8*)(buf + r * 128 + fwd_swz(r, c) * 16);
+        a[mb][u] = *(const INFCL_LDS f32x4*)(buf + r * 128 + fwd_swz(r, c) * 16);
       }
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb) {
         int r = 32 * nb + l32;
-        bb[nb] = *(const INFCL_LDS bf16x8*)(buf + r * 128 + fwd_swz(r, c) * 16);
+        bb[nb][u] = *(const INFCL_LDS f32x4*)(buf + r * 128 + fwd_swz(r, c) * 16);
       }
+    }
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb)
-          acc[mb][nb] = mfma16<std::is_same<TIN, _Float16>::value>(a[mb], bb[nb], acc[mb][nb]);
-    }
-  } else {
-    // fp32: a 16-wide contraction step is 64 bytes; lane half h holds floats 8h..8h+7
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      f32x4 a[2][2], bb[2][2];
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int c = 4 * s + 2 * h + u;
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb) {
-          int r = kFwdBI + 64 * wave + 32 * mb + l32;
-          a[mb][u] = *(const INFCL_LDS f32x4*)(buf + r * 128 + fwd_swz(r, c) * 16);
-        }
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
-          int r = 32 * nb + l32;
-          bb[nb][u] = *(const INFCL_LDS f32x4*)(buf + r * 128 + fwd_swz(r, c) * 16);
-        }
-      }
-#pragma unroll
-      for (int t = 0; t < 8; ++t)
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-          for (int nb = 0; nb < 2; ++nb)
-            acc[mb][nb] = mfma_f32(a[mb][t >> 2][t & 3], bb[nb][t >> 2][t & 3], acc[mb][nb]);
-    }
+          acc[mb][nb] = mfma_f32(a[mb][t >> 2][t & 3], bb[nb][t >> 2][t & 3], acc[mb][nb]);
   }
 }
 
@@ -311,7 +285,6 @@ __device__ __forceinline__ void fwd_epilogue(const FwdParams& p, const f32x16 (&
   }
 }
 
-template <typename TIN>
 __global__ void __launch_bounds__(256, 2) fwd_sweep(FwdParams p) {
   __shared__ __attribute__((aligned(1024))) char lds_[2 * kFwdStageBytes];
   INFCL_LDS char* lds0 = (INFCL_LDS char*)lds_;
@@ -320,7 +293,7 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep(FwdParams p) {
   const int wave = threadIdx.x >> 6;
   const int l32 = lane & 31, h = lane >> 5;
   const int64_t b = p.b;
-  const int nst = (int)((p.d * (int64_t)sizeof(TIN)) / 128);  // K-stages per tile (even)
+  const int nst = (int)((p.d * (int64_t)sizeof(float)) / 128);  // K-stages per tile (even)
 
   const int g = blockIdx.x % p.Pc;
   const int q = blockIdx.x / p.Pc;
@@ -341,9 +314,9 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep(FwdParams p) {
     rowL[nb] = 0.f;
   }
 
-  const FwdDmaOffsets dmo = fwd_dma_offsets(p.d, (int)sizeof(TIN), wave, lane);
+  const FwdDmaOffsets dmo = fwd_dma_offsets(p.d, (int)sizeof(float), wave, lane);
   int rr = 0, cc = 0;  // position of the current tile in this workgroup's (row, column) sweep
-  fwd_stage_dma<TIN>(p, dmo, p.r0 + (int64_t)q * kFwdBI, (int64_t)ct_lo * kFwdBJ, 0, lds0, wave);
+  fwd_stage_dma(p, dmo, p.r0 + (int64_t)q * kFwdBI, (int64_t)ct_lo * kFwdBJ, 0, lds0, wave);
   wait_dma();
   __syncthreads();
 
@@ -365,15 +338,15 @@ __global__ void __launch_bounds__(256, 2) fwd_sweep(FwdParams p) {
         for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
 
     for (int st = 0; st < nst; st += 2) {
-      fwd_stage_dma<TIN>(p, dmo, i0, j0, st + 1, lds1, wave);
-      fwd_stage_mfma<TIN>(lds0, acc, wave, lane);
+      fwd_stage_dma(p, dmo, i0, j0, st + 1, lds1, wave);
+      fwd_stage_mfma(lds0, acc, wave, lane);
       wait_dma();
       __syncthreads();
       if (st + 2 < nst)
-        fwd_stage_dma<TIN>(p, dmo, i0, j0, st + 2, lds0, wave);
+        fwd_stage_dma(p, dmo, i0, j0, st + 2, lds0, wave);
       else if (has_next)
-        fwd_stage_dma<TIN>(p, dmo, ni0, nj0, 0, lds0, wave);
-      fwd_stage_mfma<TIN>(lds1, acc, wave, lane);
+        fwd_stage_dma(p, dmo, ni0, nj0, 0, lds0, wave);
+      fwd_stage_mfma(lds1, acc, wave, lane);
       if (st + 2 < nst) {
         wait_dma();
         __syncthreads();
@@ -611,13 +584,8 @@ static int launch_fwd1(const void* img, const void* txt, int64_t b, int64_t d, i
   p.rstride = nrows;
   *nrowpart = p.Pc * 4;
   *ncolpart = p.Pr;
-  dim3 grid(p.Pr * p.Pc);
-  if (dtype == 0)
-    hipLaunchKernelGGL(fwd_sweep<__bf16>, grid, dim3(256), 0, stream, p);
-  else if (dtype == 2)
-    hipLaunchKernelGGL(fwd_sweep<_Float16>, grid, dim3(256), 0, stream, p);
-  else
-    hipLaunchKernelGGL(fwd_sweep<float>, grid, dim3(256), 0, stream, p);
+  if (dtype != 1) return 2;  // every supported 16-bit width takes the resident-rows sweep
+  hipLaunchKernelGGL(fwd_sweep, dim3(p.Pr * p.Pc), dim3(256), 0, stream, p);
   return hipGetLastError() == hipSuccess ? 0 : 1;
 }
 

@@ -232,7 +232,7 @@ __global__ void __launch_bounds__(64 * fwd2_waves(D), D > 512 ? 1 : 2) fwd_sweep
   // of zero bytes loads zeros)
   auto issue_slot = [&](int jt, bool first_rb, INFCL_LDS float* slot) {
     const int j0 = (jt < 0 ? 0 : jt) * kSweepBN;
-    const int nb = jt < 0 ? 0 : (b - j0) * 4;
+    const int64_t nb = jt < 0 ? 0 : (int64_t)(b - j0) * 4;
     const uint32_t so = 16u * (uint32_t)(opaque_lane() & 7);
     dma16_asm(rsrc_words(first_rb ? p.ref2 + j0 : cR + j0, nb), slot, so);
     dma16_asm(rsrc_words(cL + j0, first_rb ? 0 : nb), slot + 256, so);

@@ -52,6 +52,22 @@ def test_workspace_size_is_linear_in_b():
     assert _ws(1, 128, infcl.INFCL_BF16)[0] == infcl.INFCL_OK
 
 
+@pytest.mark.parametrize("d,dt,per_sample", [
+    # 16-bit inputs, resident-rows forward: 8 row and 32 column partial pairs
+    # (8 B each), diagonal, base-2 diagonal reference, 2 base-2 log-sum-exp values
+    (512, 0, (8 + 32) * 8 + 4 + 4 + 8), (768, 0, (8 + 32) * 8 + 4 + 4 + 8), (1024, 2, (8 + 32) * 8 + 4 + 4 + 8),
+    # fp32 inputs, streamed forward: 32 row and 64 column partial pairs, no reference
+    (512, 1, (32 + 64) * 8 + 4 + 8),
+])
+def test_workspace_bytes_per_sample(d, dt, per_sample):
+    """The workspace holds what the launched grid writes, nothing more: the
+    per-sample regions above plus per-workgroup partials (under 1 B/sample)."""
+    b = 1 << 20
+    st, w = _ws(b, d, dt)
+    assert st == infcl.INFCL_OK
+    assert per_sample * b <= w <= per_sample * b + b
+
+
 @pytest.mark.parametrize("b,d,dt,expect", [
     (0, 512, 0, infcl.INFCL_ERR_INVALID), (-3, 512, 0, infcl.INFCL_ERR_INVALID), (16, 0, 0, infcl.INFCL_ERR_INVALID),
     (16, 512, 7, infcl.INFCL_ERR_INVALID), (16, 100, 0, infcl.INFCL_ERR_UNSUPPORTED),
