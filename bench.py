@@ -7,7 +7,12 @@ gradient sweeps and dscale) over one batch of synthetic CLIP-shaped embeddings
 already resident in HBM.  The metric is similarity entries per second,
 b^2 / (time of one forward + backward).
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3]
+
+The default workload is b = 131072 pairs, d = 768, bf16, s = 100 (the largest
+of the five configurations whose default run, 20 timed steps, finishes in a few
+minutes; b = 1048576 and b = 4194304 take 8 s and 2 min per step and are run
+with --config 4 / 5 and fewer steps).
 
 Prints one JSON line.  Only one GPU is used; --gpus above 1 exits with a message.
 """
@@ -27,6 +32,7 @@ sys.path.insert(0, ROOT)
 
 BF16_PEAK = 2.5e15      # MI355X dense bf16 MFMA, FLOP/s
 FP32_MFMA_PEAK = 157.3e12
+HBM_PEAK = 8.0e12       # MI355X HBM3E, bytes/s
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
 
 
@@ -35,15 +41,16 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=2, help="workload configuration 1..5 (default 2)")
+    ap.add_argument("--config", type=int, default=3, help="workload configuration 1..5 (default 3)")
     ap.add_argument("--shards", type=int, default=1,
                     help="run each step as this many shards of the batch (one GPU's share each, "
                          "infcl_fwd_shard / _finish / infcl_bwd_shard) one after another on this device")
     ap.add_argument("--dtype", choices=["bf16", "f16", "f32"], default=None,
                     help="input type instead of the configuration's own (same shapes and scale)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-b", type=int, default=24576,
-                    help="batch size of the oracle sample timed on the host (capped at the workload b)")
+    ap.add_argument("--cpu-sample-b", type=int, default=None,
+                    help="batch size of the oracle sample timed on the host (default: the workload's b when the "
+                         "oracle finishes it in about 40 s, else the largest multiple of 4096 that does in 20 s)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 256 MiB device copy three times (reference for the HBM byte counters)")
     return ap.parse_args()
@@ -110,6 +117,18 @@ def device_info(torch):
     return info
 
 
+def cpu_sample_b(b, d):
+    """Batch size of the oracle sample: the oracle costs about 10 b^2 d fp64
+    flops plus 4 b^2 exponentials; on 16 host cores b = 24576 at d = 512 took
+    18 s.  The whole batch when that estimate is under 40 s, else the largest
+    multiple of 4096 estimated at 20 s."""
+    def est(n):
+        return 18.0 * (n / 24576.0) ** 2 * (d / 512.0)
+    if est(b) <= 40.0:
+        return b
+    return max(4096, int(24576 * math.sqrt(20.0 / 18.0 * 512.0 / d)) // 4096 * 4096)
+
+
 def cpu_baseline(cfg, sample_b):
     """The fp64 oracle (as it stands) on a bounded sample of the same workload."""
     import oracle
@@ -128,8 +147,10 @@ def cpu_baseline(cfg, sample_b):
         "unit": "entries/s",
         "cores": _threads(),
         "kind": "oracle",
-        "sample": f"full fp64 oracle forward+backward at b={sample_b} (same generator, d={cfg['d']}, "
-                  f"sigma={cfg['sigma']}, s={cfg['scale']}, seed 0): {dt:.2f} s",
+        "sample": (f"full fp64 oracle forward+backward at b={sample_b}" +
+                   (" (the whole workload)" if sample_b == cfg["b"] else
+                    f" (the first {sample_b} pairs of the b={cfg['b']} workload)") +
+                   f", same generator, d={cfg['d']}, sigma={cfg['sigma']}, s={cfg['scale']}, seed 0: {dt:.2f} s"),
     }
 
 
@@ -270,8 +291,14 @@ def main():
     workload = f"symmetric InfoNCE forward+backward, b={b} d={d} {dt_name}, sigma={cfg['sigma']}, s={cfg['scale']}"
     if a.shards > 1:
         workload += f", as {a.shards} shards"
-    src = source_hash("bwd.hip", "bwd.hpp", "sweep.hpp", "common.hpp")
+    src = source_hash("bwd.hip", "bwd_wide.hip", "bwd.hpp", "sweep.hpp", "common.hpp")
     traffic = load_traffic(bwd_kernel, workload, src)
+    # roofline bound from the arithmetic intensity: flops per HBM byte (the
+    # measured bytes when the counters are current, else the compulsory ones:
+    # both inputs read, one gradient written) against the ridge point
+    hbm_bytes = traffic if traffic else (2.0 * b * d * img.element_size() + 4.0 * b * d)
+    intensity = alg_bwd_launch / hbm_bytes
+    ridge = peak / HBM_PEAK
 
     out = {
         "metric": "similarity entries/s (b^2 per forward+backward pass)",
@@ -299,7 +326,9 @@ def main():
         "peak_hbm_bytes": int(peak_bytes - base_mem + (img.numel() + txt.numel()) * img.element_size()),
         "roofline": {
             "kernel": f"{bwd_kernel} (one of the two backward launches)",
-            "bound": "mfma",
+            "bound": "mfma" if intensity >= ridge else "hbm",
+            "intensity_flop_per_byte": intensity,
+            "ridge_flop_per_byte": ridge,
             "achieved": achieved / 1e12,
             "peak": peak / 1e12,
             "unit": "TFLOP/s",
@@ -315,7 +344,7 @@ def main():
         "device": device_info(torch),
     }
     if not a.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, min(a.cpu_sample_b, b))
+        out["cpu_baseline"] = cpu_baseline(cfg, min(a.cpu_sample_b or cpu_sample_b(b, d), b))
     print(json.dumps(out), flush=True)
 
 

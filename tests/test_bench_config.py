@@ -1,8 +1,8 @@
-"""Parity at the benchmark's full sizes, in the launch configuration bench.py
-times, on outputs the oracle can compute one by one.
+"""Parity at b = 1048576 (d = 1024, s = 50), in the launch configuration
+bench.py times, on outputs the oracle can compute one by one.
 
-For b = 32768 (d = 512, s = 14.29), b = 131072 (d = 768, s = 100) and
-b = 1048576 (d = 1024, s = 50) the full oracle takes minutes to days, so:
+(b = 32768 and b = 131072 are compared with the full oracle in
+test_full_size.py.)  Here the full oracle would take hours, so:
   * r_i, r_i - x_ii for 96 seeded rows and c_j, c_j - x_jj for 96 seeded
     columns come from the exact sampled oracle (independent of the GPU);
   * dimg rows / dtxt rows for the same indices are recomputed in fp64 from the
@@ -32,7 +32,7 @@ def _grad_rows(A, B, s, rows, lse_own_rows, lse_other_all, ell_own_rows, ell_oth
     return k * (g @ B)
 
 
-@pytest.mark.parametrize("cfg", [2, 3, 4])
+@pytest.mark.parametrize("cfg", [4])
 def test_full_size_sampled(cfg):
     c = synth.WORKLOADS[cfg]
     b, d, s = c["b"], c["d"], f32_scale(c["scale"])

@@ -117,7 +117,8 @@ def test_dloss_scaling_bf16():
     _check(gpu, fwd, dI, dT, ds, s, 256, "bf16")
 
 
-@pytest.mark.parametrize("b,d", [(1, 128), (65, 128), (1025, 256), (777, 512), (777, 640), (700, 768), (600, 1024)])
+@pytest.mark.parametrize("b,d", [(1, 128), (65, 128), (1025, 256), (777, 512), (777, 640), (700, 768), (600, 1024)]
+                         + [(300, d) for d in range(128, 1025, 128)])
 def test_fp16_inputs(b, d):
     """IEEE half embeddings (the paper's mixed-precision training type): the
     resident-rows forward (8 waves at d <= 512, 4 above), the 128-row backward
@@ -132,7 +133,7 @@ def test_fp16_scales(s, sigma):
     _check(gpu, fwd, dI, dT, ds, s32, 512, "f16")
 
 
-@pytest.mark.parametrize("b,d", [(1, 64), (17, 64), (300, 192), (1024, 512)])
+@pytest.mark.parametrize("b,d", [(1, 64), (17, 64), (1024, 512)] + [(300, d) for d in range(64, 513, 64)])
 def test_fp32_inputs(b, d):
     gpu, fwd, dI, dT, ds, s = _case(b, d, 1.0 / 0.07, dtype="f32", seed=b)
     _check(gpu, fwd, dI, dT, ds, s, d, "f32")
@@ -145,11 +146,23 @@ def test_config1_fp32_workload():
     _check(gpu, fwd, dI, dT, ds, s, c["d"], "f32")
 
 
-def test_deterministic_bitwise():
-    img, txt = synth.clip_pairs(3000, 256, 1.0, seed=11, dtype="bf16")
-    a = run(img, txt, "bf16", 14.29)
-    b = run(img, txt, "bf16", 14.29)
-    for k in ("loss64", "dscale"):
-        assert a[k] == b[k]
-    for k in ("lse_r", "lse_c", "ell_r", "ell_c", "dI", "dT"):
-        assert np.array_equal(a[k], b[k]), k
+@pytest.mark.parametrize("d", [8, 72, 200, 1000])
+def test_zero_padded_features_bf16(d):
+    """16-bit widths that are not a multiple of 128 are run by padding the
+    features with zeros up to the next multiple: zero features add nothing to
+    any dot product, so loss, r, c and dscale are those of the unpadded batch,
+    the gradients' first d columns are its gradients and the padding columns'
+    gradients are exactly zero.  Checked against the oracle at the unpadded d."""
+    b = 513
+    img, txt = synth.clip_pairs(b, d, 1.0, seed=d, dtype="bf16")
+    dp = -(-d // 128) * 128
+    pi = np.zeros((b, dp), dtype=np.uint16)
+    pt = np.zeros((b, dp), dtype=np.uint16)
+    pi[:, :d] = img
+    pt[:, :d] = txt
+    s = f32_scale(14.29)
+    gpu = run(pi, pt, "bf16", s)
+    fwd, dI, dT, ds = oracle.forward_backward(synth.as_f64(img, "bf16"), synth.as_f64(txt, "bf16"), s)
+    assert np.all(gpu["dI"][:, d:] == 0) and np.all(gpu["dT"][:, d:] == 0)
+    gpu["dI"], gpu["dT"] = gpu["dI"][:, :d], gpu["dT"][:, :d]
+    _check(gpu, fwd, dI, dT, ds, s, d, "bf16")
