@@ -152,6 +152,22 @@ infcl_status infcl_bwd_shard(const void* img, const void* txt, int64_t b, int64_
                              float* dimg, float* dtxt, double* dscale_part,
                              void* workspace, size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): infcl_fwd
+ * without the workspace arguments.  The workspace is a fixed 32 MiB array in
+ * the library's device code, one per device, held until the process ends; its
+ * address is looked up (hipGetSymbolAddress) on the first call on each device.
+ * No allocation of any kind happens.  The outputs and their meaning are those
+ * of infcl_fwd, bit for bit.  Returns INFCL_ERR_WORKSPACE when
+ * infcl_workspace_size(b, d, dtype) exceeds 32 MiB (about b = 99,000 for
+ * 16-bit inputs, b = 43,000 for f32), INFCL_ERR_HIP if the scratch address
+ * cannot be obtained.  Every call on one device shares that device's scratch:
+ * calls that overlap in time on one device (two streams, two host threads)
+ * race and give wrong results; calls in one stream order are safe. */
+infcl_status infcl_fwd_noalloc(const void* img, const void* txt, int64_t b, int64_t d, int dtype,
+                               const float* scale, float* loss, double* loss64, float* lse_r, float* lse_c,
+                               float* aux, void* stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* infcl_status_str(int status);
 

@@ -8,6 +8,7 @@ built, or no GPU is present, calls raise.
 Entry points with the C ABI's names (tensors in, status checked):
     infcl_workspace_size(b, d, dtype) -> int
     infcl_fwd(img, txt, scale, loss, loss64, lse_r, lse_c, aux, workspace)
+    infcl_fwd_noalloc(img, txt, scale, loss, loss64, lse_r, lse_c, aux)
     infcl_bwd(img, txt, scale, lse_r, lse_c, aux, dloss, dimg, dtxt, dscale, workspace)
 Convenience wrappers that allocate outputs with torch:
     clip_loss_fwd(img, txt, scale) -> dict
@@ -55,6 +56,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.infcl_workspace_size.restype = ip
     lib.infcl_fwd.argtypes = [vp, vp, i64, i64, ip, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.infcl_fwd.restype = ip
+    lib.infcl_fwd_noalloc.argtypes = [vp, vp, i64, i64, ip, vp, vp, vp, vp, vp, vp, vp]
+    lib.infcl_fwd_noalloc.restype = ip
     lib.infcl_bwd.argtypes = [vp, vp, i64, i64, ip, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.infcl_bwd.restype = ip
     lib.infcl_fwd_shard.argtypes = [vp, vp, i64, i64, ip, i64, i64, vp, vp, vp, sz, vp]
@@ -122,6 +125,13 @@ def infcl_fwd(img, txt, scale, loss, loss64, lse_r, lse_c, aux, workspace):
     _check(load_library().infcl_fwd(_ptr(img), _ptr(txt), b, d, _dtype_code(img), _ptr(scale), _ptr(loss),
                                      _ptr(loss64), _ptr(lse_r), _ptr(lse_c), _ptr(aux), _ptr(workspace),
                                      workspace.numel() * workspace.element_size(), _stream(img)), "infcl_fwd")
+
+
+def infcl_fwd_noalloc(img, txt, scale, loss, loss64, lse_r, lse_c, aux):
+    b, d = img.shape
+    _check(load_library().infcl_fwd_noalloc(_ptr(img), _ptr(txt), b, d, _dtype_code(img), _ptr(scale), _ptr(loss),
+                                             _ptr(loss64), _ptr(lse_r), _ptr(lse_c), _ptr(aux), _stream(img)),
+           "infcl_fwd_noalloc")
 
 
 def infcl_bwd(img, txt, scale, lse_r, lse_c, aux, dloss, dimg, dtxt, dscale, workspace):

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "infcl.h"
 
 namespace infcl {
@@ -87,6 +89,30 @@ bool shard_ok(int64_t b, int64_t r0, int64_t bs) { return r0 >= 0 && r0 % 32 == 
 
 constexpr int64_t kMaxParts = 1 << 16;  // shards whose column pairs one finish merges
 
+// ---- fixed scratch of infcl_fwd_noalloc: its workspace, for callers that
+// cannot allocate.  Each device holds its own copy for the life of the
+// process.  In host code the array's name is not a device address: the
+// address comes from hipGetSymbolAddress, once per device, with that device
+// current, and only that address is handed to kernels.
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) char scratch[kScratchBytes];
+void* g_scratch_ptr[kMaxDevices] = {};
+std::mutex g_scratch_mu;
+
+// The current device's scratch address (nullptr on a HIP error).
+void* scratch_address() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return nullptr;
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
 }  // namespace
 
 extern "C" {
@@ -110,6 +136,25 @@ infcl_status infcl_fwd(const void* img, const void* txt, int64_t b, int64_t d, i
   const Layout L = make_layout(b, d, dtype);
   if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)workspace;
+  int rc = infcl::launch_fwd(img, txt, b, d, dtype, scale, loss, loss64, lse_r, lse_c, aux, (hipStream_t)stream,
+                             (float*)(ws + L.rowR), (float*)(ws + L.rowL), (float*)(ws + L.colR),
+                             (float*)(ws + L.colL), (float*)(ws + L.udiag), (float*)(ws + L.ref2),
+                             (double*)(ws + L.fwd_part));
+  return rc == 0 ? INFCL_OK : INFCL_ERR_HIP;
+}
+
+infcl_status infcl_fwd_noalloc(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale,
+                               float* loss, double* loss64, float* lse_r, float* lse_c, float* aux, void* stream) {
+  if (!shape_ok(b, d, dtype)) return INFCL_ERR_INVALID;
+  if (!aligned(img, 16) || !aligned(txt, 16) || !aligned(scale, 4) || !aligned(loss, 4) || !aligned(lse_r, 16) ||
+      !aligned(lse_c, 16) || !aligned(aux, 16))
+    return INFCL_ERR_INVALID;
+  if (loss64 != nullptr && ((uintptr_t)loss64 % 8) != 0) return INFCL_ERR_INVALID;
+  if (!shape_supported(b, d, dtype)) return INFCL_ERR_UNSUPPORTED;
+  const Layout L = make_layout(b, d, dtype);
+  if (L.total > kScratchBytes) return INFCL_ERR_WORKSPACE;
+  char* ws = (char*)scratch_address();
+  if (ws == nullptr) return INFCL_ERR_HIP;
   int rc = infcl::launch_fwd(img, txt, b, d, dtype, scale, loss, loss64, lse_r, lse_c, aux, (hipStream_t)stream,
                              (float*)(ws + L.rowR), (float*)(ws + L.rowL), (float*)(ws + L.colR),
                              (float*)(ws + L.colL), (float*)(ws + L.udiag), (float*)(ws + L.ref2),

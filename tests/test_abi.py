@@ -26,7 +26,7 @@ def test_ablation_header_symbol_exported(lib):
 def test_exports_every_declared_function(lib):
     names = infcl.header_functions()
     assert set(names) == {"infcl_workspace_size", "infcl_fwd", "infcl_bwd", "infcl_status_str", "infcl_fwd_shard",
-                          "infcl_fwd_shard_finish", "infcl_bwd_shard"}
+                          "infcl_fwd_shard_finish", "infcl_bwd_shard", "infcl_fwd_noalloc"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -107,6 +107,23 @@ def _bwd(lib, img=A, txt=A, b=64, d=512, dt=0, scale=A, lr=A, lc=A, aux=A, dloss
 ])
 def test_fwd_validation(lib, kw, expect):
     assert _fwd(lib, **kw) == expect
+
+
+def _fwd_noalloc(lib, img=A, txt=A, b=64, d=512, dt=0, scale=A, loss=A, loss64=A, lr=A, lc=A, aux=A):
+    return lib.infcl_fwd_noalloc(img, txt, b, d, dt, scale, loss, loss64, lr, lc, aux, None)
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(img=None), infcl.INFCL_ERR_INVALID), (dict(txt=A + 8), infcl.INFCL_ERR_INVALID),
+    (dict(scale=None), infcl.INFCL_ERR_INVALID), (dict(loss=None), infcl.INFCL_ERR_INVALID),
+    (dict(loss64=A + 4), infcl.INFCL_ERR_INVALID), (dict(lc=A + 4), infcl.INFCL_ERR_INVALID),
+    (dict(b=0), infcl.INFCL_ERR_INVALID), (dict(dt=3), infcl.INFCL_ERR_INVALID),
+    (dict(d=96), infcl.INFCL_ERR_UNSUPPORTED),
+    # the fixed 32 MiB scratch: 16-bit inputs need 336 B per sample, f32 780 B
+    (dict(b=100000), infcl.INFCL_ERR_WORKSPACE), (dict(b=50000, d=256, dt=1), infcl.INFCL_ERR_WORKSPACE),
+])
+def test_fwd_noalloc_validation(lib, kw, expect):
+    assert _fwd_noalloc(lib, **kw) == expect
 
 
 @pytest.mark.parametrize("kw,expect", [

@@ -1,0 +1,58 @@
+"""The allocation-free forward (infcl_fwd_noalloc: infcl_fwd with its
+workspace in the library's fixed per-device scratch) against infcl_fwd with a
+caller workspace, through the C ABI: two calls in a row, the second with a
+smaller batch (the scratch then holds the first call's data), each equal bit
+for bit to infcl_fwd on the same inputs (the same kernels and the same order
+of operations); and the size limit is reported, not run."""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2410_17243_amd as infcl
+from gpu_util import device_inputs, f32_scale, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _outputs(b, dev):
+    return {"loss": torch.empty((), dtype=torch.float32, device=dev),
+            "loss64": torch.empty((), dtype=torch.float64, device=dev),
+            "lse_r": torch.empty(b, dtype=torch.float32, device=dev),
+            "lse_c": torch.empty(b, dtype=torch.float32, device=dev),
+            "aux": torch.empty(3 * b, dtype=torch.float32, device=dev)}
+
+
+def _np(o):
+    return {k: v.cpu().numpy() for k, v in o.items()}
+
+
+@pytest.mark.parametrize("d,dtype", [(512, "bf16"), (768, "bf16"), (256, "f32")])
+def test_noalloc_forward_matches_workspace_forward(d, dtype):
+    s = f32_scale(14.29)
+    for b in (5000, 1337):  # the second call is smaller
+        img, txt = synth.clip_pairs(b, d, 1.0, seed=b + d, dtype=dtype)
+        I, T = device_inputs(img, txt, dtype)
+        sc = torch.tensor(s, dtype=torch.float32, device=I.device)
+        ref = _outputs(b, I.device)
+        infcl.infcl_fwd(I, T, sc, ref["loss"], ref["loss64"], ref["lse_r"], ref["lse_c"], ref["aux"],
+                        infcl.workspace_for(I))
+        got = _outputs(b, I.device)
+        infcl.infcl_fwd_noalloc(I, T, sc, got["loss"], got["loss64"], got["lse_r"], got["lse_c"], got["aux"])
+        torch.cuda.synchronize()
+        r, g = _np(ref), _np(got)
+        print(f"b={b} d={d} {dtype}: loss {float(g['loss64']):.12e} (workspace call {float(r['loss64']):.12e})",
+              flush=True)
+        for k in r:
+            assert np.array_equal(g[k], r[k]), k
+
+
+def test_noalloc_forward_rejects_batches_beyond_the_scratch():
+    b, d = 120000, 512  # 336 B per sample of workspace: over 32 MiB
+    assert infcl.infcl_workspace_size(b, d, infcl.INFCL_BF16) > 32 << 20
+    I = torch.zeros((b, d), dtype=torch.bfloat16, device="cuda")
+    sc = torch.tensor(14.29, dtype=torch.float32, device="cuda")
+    o = _outputs(b, I.device)
+    with pytest.raises(infcl.InfclError) as e:
+        infcl.infcl_fwd_noalloc(I, I, sc, o["loss"], o["loss64"], o["lse_r"], o["lse_c"], o["aux"])
+    assert e.value.status == infcl.INFCL_ERR_WORKSPACE
