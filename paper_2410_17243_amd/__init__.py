@@ -66,8 +66,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.infcl_fwd_shard_finish.restype = ip
     lib.infcl_bwd_shard.argtypes = [vp, vp, i64, i64, ip, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.infcl_bwd_shard.restype = ip
-    lib.infcl_ablation_dt_atomics.argtypes = [vp, i64, i64, i64, vp]
-    lib.infcl_ablation_dt_atomics.restype = ip
+    lib.infcl_ablation_bwd_single.argtypes = [vp, vp, i64, i64, ip, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.infcl_ablation_bwd_single.restype = ip
     lib.infcl_status_str.argtypes = [ip]
     lib.infcl_status_str.restype = ctypes.c_char_p
     _lib = lib
@@ -167,12 +167,13 @@ def infcl_bwd_shard(img, txt, scale, r0, bs, lse_r, lse_c, aux, dloss, dimg, dtx
            "infcl_bwd_shard")
 
 
-def infcl_ablation_dt_atomics(dT, bm: int):
-    """The text-gradient update traffic of a single-launch backward (include/infcl_ablation.h)."""
-    b, d = dT.shape
-    rc = load_library().infcl_ablation_dt_atomics(_ptr(dT), b, d, int(bm), _stream(dT))
-    if rc != 0:
-        raise InfclError(rc, "infcl_ablation_dt_atomics")
+def infcl_ablation_bwd_single(img, txt, scale, lse_r, lse_c, aux, dloss, dimg, dtxt, dscale, workspace):
+    """The single-launch backward with atomic text-gradient updates (include/infcl_ablation.h)."""
+    b, d = img.shape
+    _check(load_library().infcl_ablation_bwd_single(
+        _ptr(img), _ptr(txt), b, d, _dtype_code(img), _ptr(scale), _ptr(lse_r), _ptr(lse_c), _ptr(aux), _ptr(dloss),
+        _ptr(dimg), _ptr(dtxt), _ptr(dscale), _ptr(workspace), workspace.numel() * workspace.element_size(),
+        _stream(img)), "infcl_ablation_bwd_single")
 
 
 # ------------------------------------------------------------- torch wrappers

@@ -1,15 +1,15 @@
-"""Single-launch backward ablation: what the text-gradient update of the
-appendix's in-GPU backward algorithm costs on this GPU, against the two-launch
-backward of infcl_bwd.
+"""Single-launch backward ablation: the appendix's in-GPU backward (one sweep,
+each similarity tile and its softmax weights computed once, the text-gradient
+tile updated in memory for every tile, with atomics) against the two-launch
+backward of infcl_bwd (two sweeps, the similarity tile recomputed, every
+gradient written once).
 
     python -m paper_2410_17243_amd.ablation [--config 2] [--reps 5]
 
-Prints one JSON line: the two-launch backward time, the time of the dT update
-traffic alone (infcl_ablation_dt_atomics, hardware fp32 atomics) for row blocks
-of 128 rows (the most whose dI accumulators fit the register file at d = 512)
-and 256 rows, its bytes, and the HBM-bandwidth floor of the same update done as
-a plain read-modify-write (read and write of every 32 x d tile per row block at
-8 TB/s).  The update alone already bounds the single-launch backward from below.
+Prints one JSON line: the time of each backward on the workload's inputs, the
+MFMA flops each executes (the single launch 6 b^2 d, the two launches
+8 b^2 d), and the single launch's atomic payload (ceil(b / 64) additions of
+every text-gradient element).
 """
 
 from __future__ import annotations
@@ -33,17 +33,18 @@ def main(argv=None):
 
     cfg = synth.WORKLOADS[a.config]
     b, d = cfg["b"], cfg["d"]
+    if cfg["dtype"] != "bf16" or d not in (256, 512):
+        raise SystemExit("the single-launch backward covers bf16 inputs with d = 256 or 512")
     dev = torch.device("cuda:0")
-    img_np, txt_np = synth.clip_pairs(b, d, cfg["sigma"], seed=0, dtype=cfg["dtype"])
-    tdt = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[cfg["dtype"]]
-    if cfg["dtype"] == "f32":
-        img = torch.from_numpy(img_np).to(dev)
-        txt = torch.from_numpy(txt_np).to(dev)
-    else:
-        img = torch.from_numpy(img_np.view(np.int16)).view(tdt).to(dev)
-        txt = torch.from_numpy(txt_np.view(np.int16)).view(tdt).to(dev)
+    img_np, txt_np = synth.clip_pairs(b, d, cfg["sigma"], seed=0, dtype="bf16")
+    img = torch.from_numpy(img_np.view(np.int16)).view(torch.bfloat16).to(dev)
+    txt = torch.from_numpy(txt_np.view(np.int16)).view(torch.bfloat16).to(dev)
     sc = torch.tensor([cfg["scale"]], dtype=torch.float32, device=dev).reshape(())
     f = infcl.clip_loss_fwd(img, txt, sc)
+    ws = f["workspace"]
+    dimg = torch.empty((b, d), dtype=torch.float32, device=dev)
+    dtxt = torch.empty((b, d), dtype=torch.float32, device=dev)
+    ds = torch.empty((), dtype=torch.float32, device=dev)
 
     def timed(fn):
         fn()
@@ -56,22 +57,23 @@ def main(argv=None):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / a.reps
 
-    bwd_ms = timed(lambda: infcl.clip_loss_bwd(img, txt, sc, f))
-    dT = torch.zeros((b, d), dtype=torch.float32, device=dev)
-    out = {"workload": f"b={b} d={d} {cfg['dtype']}", "two_launch_backward_ms": bwd_ms, "update": []}
-    for bm in (128, 256):
-        dT.zero_()
-        ms = timed(lambda: infcl.infcl_ablation_dt_atomics(dT, bm))
-        nwg = -(-b // bm)
-        want = float(nwg * (a.reps + 1))
-        exact = bool(torch.all(dT == want).item())
-        payload = nwg * b * d * 4  # bytes added per launch
-        out["update"].append({
-            "row_block": bm, "ms": ms, "atomic_payload_GiB": payload / 2**30,
-            "payload_rate_TBps": payload / (ms * 1e-3) / 1e12,
-            "rmw_floor_ms_at_8TBps": 2 * payload / 8e12 * 1e3, "exact": exact,
-            "ratio_to_two_launch_backward": ms / bwd_ms,
-        })
+    two = timed(lambda: infcl.infcl_bwd(img, txt, sc, f["lse_r"], f["lse_c"], f["aux"], None, dimg, dtxt, ds, ws))
+    two_ds = float(ds.item())
+    one = timed(lambda: infcl.infcl_ablation_bwd_single(img, txt, sc, f["lse_r"], f["lse_c"], f["aux"], None, dimg,
+                                                        dtxt, ds, ws))
+    one_ds = float(ds.item())
+    nwg = -(-b // 64)
+    payload = nwg * b * d * 4
+    out = {
+        "workload": f"b={b} d={d} bf16, sigma={cfg['sigma']}, s={cfg['scale']}",
+        "two_launch_backward_ms": two,
+        "single_launch_backward_ms": one,
+        "ratio_single_to_two": one / two,
+        "executed_mfma_tflop": {"two_launch": 8.0 * b * b * d / 1e12, "single_launch": 6.0 * b * b * d / 1e12},
+        "single_launch_atomic_payload_GiB": payload / 2**30,
+        "single_launch_atomic_payload_rate_TBps": payload / (one * 1e-3) / 1e12,
+        "dscale": {"two_launch": two_ds, "single_launch": one_ds},
+    }
     print(json.dumps(out), flush=True)
     return 0
 

@@ -293,6 +293,307 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
   if (threadIdx.x == 0) p.ds_part[blockIdx.x] = red[0];
 }
 
+// ---------------------------------------------------------------------------
+// Pipelined form for d = 768, where three swept tiles fit in LDS (3 x 48 KiB).
+// Same quantities and the same per-entry arithmetic as bwd_wide; the work of
+// three tiles overlaps in each iteration t, with two barriers per tile:
+//   stage 1  GEMM1 of tile t+1 (partial S^T over the wave's feature half),
+//            with the G' entries of tile t (joined in the previous stage 2)
+//            computed between its MFMAs: exponentials issued among MFMAs of
+//            the same wave cost little up to about two per MFMA, where the
+//            serial form spends a phase without MFMAs on them;
+//            then G' of tile t into the G' block, the partner's half of tile
+//            t+1 into the join area, and the DMA of tile t+2.  The DMA sits in
+//            this phase without MFMAs on purpose: issued among either stage's
+//            MFMAs, its LDS writes slowed the stage's LDS operand reads so
+//            much that each 1 KiB instruction cost about 200 cycles (phase
+//            trace at d = 768), against about 95 here;
+//   barrier  (G' block of tile t complete, join data of tile t+1 visible)
+//   stage 2  GEMM2 of tile t, then the read of the partner's half of tile t+1;
+//            wait for the DMA;
+//   barrier  (tile t+2 landed; tile t's buffer, the G' block and the join
+//            area are free).
+// A tile's buffer is written by its DMA in iteration t-2 (after the barrier
+// that ends iteration t-3, i.e. after the last reads of the tile three places
+// earlier), read by GEMM1 in iteration t-1 and by GEMM2 in iteration t.
+// At d = 1024 three tiles (3 x 64 KiB) do not fit in LDS: bwd_wide serves it.
+template <int D, bool F16>
+__global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
+  constexpr int KS = D / 16;
+  constexpr int KH = KS / 2;
+  constexpr int ROWG = D * 2;
+  constexpr int TILEB = kBwdBN * ROWG;
+  constexpr int NIW = TILEB / 4096;  // 1 KiB DMA instructions per wave and tile
+  constexpr int FBW = D / 128;       // 32-feature blocks of GEMM2 per wave
+  constexpr int kPre = 4;
+  constexpr int NG = 2 * FBW;  // GEMM2 groups
+  static_assert(KH % 8 == 0 && KH >= 8, "feature halves start on a 128-feature segment");
+  static_assert(3 * TILEB + 3 * 1024 + kWideBM * kBwdBN * 2 + 4 * 64 * 8 * 4 <= 160 * 1024, "LDS budget");
+  __shared__ __attribute__((aligned(1024))) char tiles_[3 * TILEB];
+  __shared__ __attribute__((aligned(1024))) float lses_[3 * 256];
+  __shared__ __attribute__((aligned(1024))) char gp_[kWideBM * kBwdBN * 2];
+  __shared__ __attribute__((aligned(16))) float xs_[4][64][8];
+  INFCL_LDS char* const tiles = (INFCL_LDS char*)tiles_;
+  INFCL_LDS float* const lses = (INFCL_LDS float*)lses_;
+  INFCL_LDS char* const gp = (INFCL_LDS char*)gp_;
+
+  const int lane = __lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int ob = wave >> 1, kh = wave & 1;
+  const int l32 = lane & 31, h = lane >> 5;
+  const int64_t b = p.b;
+  const int64_t wg0 = p.own_off + (int64_t)blockIdx.x * kWideBM;
+  const int64_t own0 = wg0 + 32 * ob;
+  const int64_t iown = own0 + l32;
+  const bool own_ok = iown < p.own_end;
+  const int64_t irow = own_ok ? iown : p.own_end - 1;
+  const bool wave_rows_ok = own0 + 32 <= p.own_end;
+  const int ntile = (int)((b + kBwdBN - 1) / kBwdBN);
+
+  const float s = p.scale[0];
+  const float k2 = s * kLog2e;
+  const float dl = p.dloss ? p.dloss[0] : 1.0f;
+  const float g16a = F16 ? p.g16[0] : 1.0f;
+  const float kfin = dl * s / (2.0f * (float)b) * (F16 ? p.g16[1] : 1.0f);
+
+  bf16x8 ownf[KH];
+  {
+    const __bf16* src = (const __bf16*)p.own + irow * D + kh * (D / 2) + 8 * h;
+#pragma unroll
+    for (int s2 = 0; s2 < KH; ++s2) ownf[s2] = *(const bf16x8*)(src + 16 * s2);
+  }
+  const float aO = own_ok ? p.lse_own[iown] * kLog2e : 0.f;
+  const float uO = own_ok ? p.udiag[iown] : 0.f;
+  const float gdiag = own_ok ? expm1f(-p.ell_own[iown]) + expm1f(-p.ell_swept[iown]) : 0.f;
+
+  auto opaque_lane = [&]() {
+    int lo = lane;
+    asm volatile("" : "+v"(lo));
+    return lo;
+  };
+  auto tile_rsrc = [&](int jt) {
+    const int64_t j0 = (int64_t)(jt < 0 ? 0 : jt) * kBwdBN;
+    return rsrc_words((const char*)p.swept + j0 * ROWG, jt < 0 ? 0 : (b - j0) * ROWG);
+  };
+  auto lse_rsrc = [&](int jt) {
+    const int64_t j0 = (int64_t)(jt < 0 ? 0 : jt) * kBwdBN;
+    return rsrc_words(p.lse2_swept + j0, jt < 0 ? 0 : (b - j0) * 4);
+  };
+  auto tbuf = [&](int t) { return tiles + TILEB * (t % 3); };
+  auto lbuf = [&](int t) { return lses + 256 * (t % 3); };
+  // DMA instruction kk of tile jt into its buffer; kk == NIW is the
+  // log-sum-exp slot (8 copies of the tile's 32 values, all waves alike)
+  auto dma_part = [&](int jt, int kk) {
+    if (kk < NIW) {
+      const uint32_t lo = sweep_dma_lane_off(opaque_lane(), wave, ROWG);
+      dma16_asm(tile_rsrc(jt < ntile ? jt : -1), tbuf(jt) + 1024 * (wave + 4 * kk), lo + sweep_dma_kk_off(kk, wave, ROWG));
+    } else {
+      dma16_asm(lse_rsrc(jt < ntile ? jt : -1), lbuf(jt), 16u * (uint32_t)(opaque_lane() & 7));
+    }
+  };
+
+  double ds_acc = 0.0;
+  f32x16 dacc[2 * FBW];
+#pragma unroll
+  for (int i = 0; i < 2 * FBW; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dacc[i][r] = 0.f;
+
+  // G' entry of the lane's own row against swept row with base-2 LSE Lj
+  auto gp_entry = [&](float x, float Lj, float& ds) {
+    const float pO = exp2_hw(__builtin_fmaf(x, k2, -aO));
+    const float pS = exp2_hw(__builtin_fmaf(x, k2, -Lj));
+    ds = __builtin_fmaf(pO, x - uO, ds);
+    return F16 ? (pO + pS) * g16a : pO + pS;
+  };
+
+  // ---- stage 1: GEMM1 of tile t1 (partial S^T over this wave's feature
+  // half); between its MFMAs, the G' entries of tile t from the joined values
+  // x (LSE values L0, L1 read from tile t's slot).  Returns the accumulator
+  // of tile t1.
+  auto stage1 = [&](int t1, const float (&x)[8], const f32x4& L0, const f32x4& L1, float (&gv)[8], float& ds_t,
+                    bool with_gp) {
+    int offA[8];
+    {
+      const int lo = opaque_lane();
+      const int rA = sweep_perm(lo & 31);
+      const int gA = sweep_g(rA);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) offA[k] = rA * kSegRow + 16 * ((2 * k + (lo >> 5)) ^ gA);
+    }
+    const INFCL_LDS char* half = tbuf(t1) + kSeg * (kh * KH / 8);
+    f32x16 sacc;
+    bf16x8 ring[kPre];
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) ring[i] = *(const INFCL_LDS bf16x8*)(half + offA[i & 7] + kSeg * (i >> 3));
+    __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
+#pragma unroll
+    for (int s2 = 0; s2 < KH; ++s2) {
+      mfma16_vgpr<F16>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KH - 1);
+      if (s2 + kPre < KH) {
+        const int n = s2 + kPre;
+        ring[s2 % kPre] = *(const INFCL_LDS bf16x8*)(half + offA[n & 7] + kSeg * (n >> 3));
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      if (with_gp && s2 % 3 == 1) {
+        const int i = s2 / 3;  // 8 entries over the 24 MFMAs
+        gv[i] = gp_entry(x[i], i < 4 ? L0[i] : L1[i - 4], ds_t);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    return sacc;
+  };
+
+  // ---- stage 2: GEMM2 of tile t (all 64 own rows' G' x this wave's quarter of
+  // the tile's features, transposing reads two groups ahead)
+  auto stage2 = [&](int t) {
+    const INFCL_LDS char* cur = tbuf(t);
+    const int lo = opaque_lane();
+    const int l32o = lo & 31, ho = lo >> 5;
+    const int g4 = lo >> 4, l16 = lo & 15;
+    const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
+    const int lb = 2 * nb16 + (qq >> 1);
+    const int fo = (qq & 1) * 8;
+    const int gpo = l32o * 64;
+    const int gsw = (l32o >> 2) & 3;
+    auto readB = [&](int g, s16x4 (&bq)[2]) {
+      const int s2 = g / FBW, fbabs = wave * FBW + g % FBW;
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt) {
+        const int off = (8 * hh + 4 * tt + e + 16 * s2) * kSegRow + kSeg * (fbabs >> 2) +
+                        16 * (4 * ((fbabs & 3) ^ e) + (lb ^ ((tt + 2 * hh) & 3))) + fo;
+        bq[tt] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFCL_LDS s16x4*)(cur + off));
+      }
+    };
+    bf16x8 A[2];
+    s16x4 bq[3][2];
+    readB(0, bq[0]);
+    readB(1, bq[1]);
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const int s2 = g / FBW, fbw = g % FBW;
+      if (fbw == 0) {
+#pragma unroll
+        for (int o2 = 0; o2 < 2; ++o2)
+          A[o2] = *(const INFCL_LDS bf16x8*)(gp + 2048 * o2 + gpo + 16 * ((2 * s2 + ho) ^ gsw));
+      }
+      if (g + 2 < NG) readB(g + 2, bq[(g + 2) % 3]);
+      const s16x4* q = bq[g % 3];
+      const s16x8 bb = {q[0][0], q[0][1], q[0][2], q[0][3], q[1][0], q[1][1], q[1][2], q[1][3]};
+#pragma unroll
+      for (int o2 = 0; o2 < 2; ++o2)
+        dacc[o2 * FBW + fbw] = mfma16<F16>(A[o2], __builtin_bit_cast(bf16x8, bb), dacc[o2 * FBW + fbw]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  // ---- prologue: tiles 0 and 1 in flight, GEMM1 of tile 0, its join
+  float x[8];
+  {
+#pragma unroll
+    for (int kk = 0; kk <= NIW; ++kk) dma_part(0, kk);
+#pragma unroll
+    for (int kk = 0; kk <= NIW; ++kk) dma_part(1, kk);
+    wait_dma();
+    __syncthreads();
+    float gv0[8], ds0 = 0.f;
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    float x0[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    const f32x16 sacc = stage1(0, x0, z, z, gv0, ds0, false);
+    float mine[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) mine[i] = kh ? sacc[8 + i] : sacc[i];
+    *(INFCL_LDS f32x4*)&xs_[wave][lane][0] = f32x4{kh ? sacc[0] : sacc[8], kh ? sacc[1] : sacc[9],
+                                                   kh ? sacc[2] : sacc[10], kh ? sacc[3] : sacc[11]};
+    *(INFCL_LDS f32x4*)&xs_[wave][lane][4] = f32x4{kh ? sacc[4] : sacc[12], kh ? sacc[5] : sacc[13],
+                                                   kh ? sacc[6] : sacc[14], kh ? sacc[7] : sacc[15]};
+    __syncthreads();
+    const f32x4 q0 = *(const INFCL_LDS f32x4*)&xs_[wave ^ 1][lane][0];
+    const f32x4 q1 = *(const INFCL_LDS f32x4*)&xs_[wave ^ 1][lane][4];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = mine[i] + (i < 4 ? q0[i] : q1[i - 4]);
+    __syncthreads();
+  }
+
+  for (int t = 0; t < ntile; ++t) {
+    // ---- stage 1
+    float mine[8];
+    {
+      const INFCL_LDS float* lp = lbuf(t) + 16 * kh + 8 * h;
+      const f32x4 L0 = *(const INFCL_LDS f32x4*)lp;
+      const f32x4 L1 = *(const INFCL_LDS f32x4*)(lp + 4);
+      float gv[8], ds_t = 0.f;
+      const f32x16 sacc = stage1(t + 1, x, L0, L1, gv, ds_t, true);
+      const int64_t j0 = (int64_t)t * kBwdBN;
+      if ((j0 == own0) || (j0 + kBwdBN > b) || !wave_rows_ok) {
+        // tile on the diagonal or past the ragged end: masked entries
+        ds_t = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int64_t j = j0 + 16 * kh + 8 * h + i;
+          const float Lj = i < 4 ? L0[i] : L1[i - 4];
+          float dsv = 0.f;
+          float gg = gp_entry(x[i], Lj, dsv);
+          const bool ok = (bool)(own_ok & (j < b));
+          const bool dg = j == iown;
+          gg = dg ? gdiag * (F16 ? g16a : 1.0f) : (ok ? gg : 0.f);
+          ds_t += (ok & !dg) ? dsv : 0.f;
+          gv[i] = gg;
+        }
+      }
+      ds_acc += (double)ds_t;
+      bf16x8 ga;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) ga[i] = to16<F16>(gv[i]);
+      const int row = 32 * ob + l32;
+      *(INFCL_LDS bf16x8*)(gp + row * 64 + 16 * ((2 * kh + h) ^ ((row >> 2) & 3))) = ga;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) mine[i] = kh ? sacc[8 + i] : sacc[i];
+      *(INFCL_LDS f32x4*)&xs_[wave][lane][0] = f32x4{kh ? sacc[0] : sacc[8], kh ? sacc[1] : sacc[9],
+                                                     kh ? sacc[2] : sacc[10], kh ? sacc[3] : sacc[11]};
+      *(INFCL_LDS f32x4*)&xs_[wave][lane][4] = f32x4{kh ? sacc[4] : sacc[12], kh ? sacc[5] : sacc[13],
+                                                     kh ? sacc[6] : sacc[14], kh ? sacc[7] : sacc[15]};
+#pragma unroll
+      for (int kk = 0; kk <= NIW; ++kk) dma_part(t + 2, kk);
+    }
+    __syncthreads();  // G' block of tile t complete; join data of tile t+1 visible
+    // ---- stage 2
+    stage2(t);
+    {
+      const f32x4 q0 = *(const INFCL_LDS f32x4*)&xs_[wave ^ 1][lane][0];
+      const f32x4 q1 = *(const INFCL_LDS f32x4*)&xs_[wave ^ 1][lane][4];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) x[i] = mine[i] + (i < 4 ? q0[i] : q1[i - 4]);
+    }
+    wait_dma();
+    __syncthreads();  // tile t+2 landed; tile t's buffer, the G' block and the join area are free
+  }
+
+  // ---- write dOwn (as bwd_wide)
+  const bool all_ok = wg0 + kWideBM <= p.own_end;
+#pragma unroll
+  for (int o2 = 0; o2 < 2; ++o2) {
+    float* dst = p.dOwn + (wg0 - p.own_off + 32 * o2 + 4 * h) * D + 32 * (wave * FBW) + l32;
+#pragma unroll
+    for (int fbw = 0; fbw < FBW; ++fbw)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = wg0 + 32 * o2 + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (all_ok || row < p.own_end) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fbw] = kfin * dacc[o2 * FBW + fbw][r];
+      }
+  }
+
+  // ---- dscale partial: fixed-order reduction in the (now free) join area
+  double* red = (double*)&xs_[0][0][0];
+  red[threadIdx.x] = ds_acc;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) p.ds_part[blockIdx.x] = red[0];
+}
+
 bool bwd_wide_supported(int64_t d, int dtype) { return (dtype == 0 || dtype == 2) && (d == 768 || d == 1024); }
 
 int bwd_wide_workgroups(int64_t nown) { return (int)((nown + kWideBM - 1) / kWideBM); }
@@ -301,9 +602,9 @@ int launch_bwd_wide(const BwdParams& p, int nwg, bool f16, hipStream_t stream) {
   switch (p.d) {
     case 768:
       if (f16)
-        hipLaunchKernelGGL((bwd_wide<768, true>), dim3(nwg), dim3(256), 0, stream, p);
+        hipLaunchKernelGGL((bwd_wide3<768, true>), dim3(nwg), dim3(256), 0, stream, p);
       else
-        hipLaunchKernelGGL((bwd_wide<768, false>), dim3(nwg), dim3(256), 0, stream, p);
+        hipLaunchKernelGGL((bwd_wide3<768, false>), dim3(nwg), dim3(256), 0, stream, p);
       break;
     case 1024:
       if (f16)

@@ -7,20 +7,28 @@ import pytest
 
 import paper_2410_17243_amd as infcl
 
+# Fake but aligned device addresses: every call below must return before any launch.
+A = 1 << 20
+
 
 @pytest.fixture(scope="module")
 def lib():
     return infcl.load_library()
 
 
+def _single(lib, img=A, txt=A, b=64, d=512, dt=0, scale=A, lr=A, lc=A, aux=A, dloss=A, di=A, dtx=A, ds=A, ws=A,
+            wsb=1 << 30):
+    return lib.infcl_ablation_bwd_single(img, txt, b, d, dt, scale, lr, lc, aux, dloss, di, dtx, ds, ws, wsb, None)
+
+
 def test_ablation_header_symbol_exported(lib):
     names = infcl.header_functions(infcl.ABLATION_HEADER_PATH)
-    assert names == ["infcl_ablation_dt_atomics"]
+    assert names == ["infcl_ablation_bwd_single"]
     assert hasattr(lib, names[0])
-    assert lib.infcl_ablation_dt_atomics(None, 64, 64, 128, None) == 1
-    assert lib.infcl_ablation_dt_atomics(A + 4, 64, 64, 128, None) == 1
-    assert lib.infcl_ablation_dt_atomics(A, 0, 64, 128, None) == 1
-    assert lib.infcl_ablation_dt_atomics(A, 64, 64, 0, None) == 1
+    assert _single(lib, img=None) == 1 and _single(lib, dtx=A + 4) == 1 and _single(lib, b=0) == 1
+    assert _single(lib, dloss=A + 2) == 1 and _single(lib, ws=A + 16) == 1
+    assert _single(lib, dt=2) == 2 and _single(lib, d=768) == 2 and _single(lib, d=128) == 2
+    assert _single(lib, wsb=16) == 3
 
 
 def test_exports_every_declared_function(lib):
@@ -84,8 +92,6 @@ def test_workspace_size_null_out(lib):
     assert lib.infcl_workspace_size(16, 512, 0, None) == infcl.INFCL_ERR_INVALID
 
 
-# Fake but aligned device addresses: every call below must return before any launch.
-A = 1 << 20
 
 
 def _fwd(lib, img=A, txt=A, b=64, d=512, dt=0, scale=A, loss=A, loss64=A, lr=A, lc=A, aux=A, ws=A, wsb=1 << 30):
