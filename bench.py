@@ -34,6 +34,7 @@ BF16_PEAK = 2.5e15      # MI355X dense bf16 MFMA, FLOP/s
 FP32_MFMA_PEAK = 157.3e12
 HBM_PEAK = 8.0e12       # MI355X HBM3E, bytes/s
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
+PROFILE_MFMA = os.path.join(ROOT, "profiles", "mfma_busy.json")
 
 
 def parse():
@@ -45,6 +46,9 @@ def parse():
     ap.add_argument("--shards", type=int, default=1,
                     help="run each step as this many shards of the batch (one GPU's share each, "
                          "infcl_fwd_shard / _finish / infcl_bwd_shard) one after another on this device")
+    ap.add_argument("--b", type=int, default=None,
+                    help="batch size instead of the configuration's own (same d, input type, noise and scale; "
+                         "used for counters that wrap on long launches)")
     ap.add_argument("--dtype", choices=["bf16", "f16", "f32"], default=None,
                     help="input type instead of the configuration's own (same shapes and scale)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -69,52 +73,59 @@ def load_traffic(kernel: str, workload: str, src: str):
     when absent or taken on a different kernel source."""
     try:
         with open(PROFILE_TRAFFIC) as f:
-            t = json.load(f)
-        e = t[kernel]
-        if e.get("source_hash") != src or e.get("workload") != workload:
-            return None
-        return e["bytes_per_launch"]
+            e = json.load(f)[f"{kernel}|{workload}"]
+        return e["bytes_per_launch"] if e.get("source_hash") == src else None
     except (OSError, KeyError, ValueError):
         return None
 
 
-def smi_reading(text: str):
-    """(sclk MHz, junction or edge temperature in C) from `rocm-smi --json`
-    output; None for what it does not hold."""
-    import re
+def load_mfma_busy(kernel: str, d: int, src: str):
+    """MFMA-pipe occupancy of the kernel at width d from the committed counter
+    runs (busy cycles over elapsed cycles at the running clock), with the
+    batch it was measured at; None when absent or taken on other source."""
     try:
-        cards = json.loads(text)
-    except ValueError:
-        return None, None
-    card = next(iter(cards.values()), {}) if isinstance(cards, dict) and cards else {}
+        with open(PROFILE_MFMA) as f:
+            e = json.load(f)[f"{kernel}|d={d}"]
+        return {"busy": e["busy"], "measured_at": e["measured_at"], "clock_ghz": e.get("clock_ghz")} \
+            if e.get("source_hash") == src else None
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def sysfs_reading():
+    """(shader clock MHz, temperature C) of card 0 from sysfs, or None where
+    absent: the clock is the starred level of pp_dpm_sclk, the temperature
+    the hottest hwmon sensor of the card.  Read from files; no program is run."""
+    import glob
+    import re
     sclk = temp = None
-    for k, v in card.items() if isinstance(card, dict) else []:
-        kl = k.lower()
-        m = re.search(r"(\d+(?:\.\d+)?)", str(v))
-        if not m:
+    for dev in sorted(glob.glob("/sys/class/drm/card*/device")):
+        try:
+            with open(os.path.join(dev, "pp_dpm_sclk")) as f:
+                for line in f:
+                    if line.rstrip().endswith("*"):
+                        m = re.search(r"(\d+)\s*[Mm][Hh]z", line)
+                        sclk = float(m.group(1)) if m else None
+            temps = []
+            for t in glob.glob(os.path.join(dev, "hwmon", "hwmon*", "temp*_input")):
+                with open(t) as f:
+                    temps.append(int(f.read().strip()) / 1000.0)
+            temp = max(temps) if temps else None
+        except (OSError, ValueError):
             continue
-        if "sclk" in kl and sclk is None:
-            sclk = float(m.group(1))
-        elif "temperature" in kl and ("junction" in kl or ("edge" in kl and temp is None)):
-            temp = float(m.group(1))
+        if sclk is not None:
+            break
     return sclk, temp
 
 
 def device_info(torch):
     """Name, architecture and CU count of device 0, and its shader clock and
-    temperature as rocm-smi reads them right after the timed steps (None
-    where the tool is missing or prints something else)."""
-    import subprocess
+    temperature right after the timed steps (None where sysfs does not show
+    them)."""
     pr = torch.cuda.get_device_properties(0)
-    info = {"name": pr.name, "arch": getattr(pr, "gcnArchName", None), "cus": pr.multi_processor_count,
-            "sclk_mhz_after": None, "temp_c_after": None}
-    try:
-        r = subprocess.run(["rocm-smi", "-d", "0", "--showclocks", "--showtemp", "--json"], capture_output=True,
-                           text=True, timeout=20)
-        info["sclk_mhz_after"], info["temp_c_after"] = smi_reading(r.stdout)
-    except (OSError, subprocess.SubprocessError):
-        pass
-    return info
+    sclk, temp = sysfs_reading()
+    return {"name": pr.name, "arch": getattr(pr, "gcnArchName", None), "cus": pr.multi_processor_count,
+            "sclk_mhz_after": sclk, "temp_c_after": temp}
 
 
 def cpu_sample_b(b, d):
@@ -179,6 +190,8 @@ def main():
     cfg = dict(synth.WORKLOADS[a.config])
     if a.dtype is not None:
         cfg["dtype"] = a.dtype
+    if a.b is not None:
+        cfg["b"] = a.b
     b, d, dt_name = cfg["b"], cfg["d"], cfg["dtype"]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -291,6 +304,7 @@ def main():
     workload = f"symmetric InfoNCE forward+backward, b={b} d={d} {dt_name}, sigma={cfg['sigma']}, s={cfg['scale']}"
     if a.shards > 1:
         workload += f", as {a.shards} shards"
+    fwd_kernel = "fwd_sweep2" if dt_name != "f32" and d % 128 == 0 and d <= 1024 else "fwd_sweep"
     src = source_hash("bwd.hip", "bwd_wide.hip", "bwd.hpp", "sweep.hpp", "common.hpp")
     traffic = load_traffic(bwd_kernel, workload, src)
     # roofline bound from the arithmetic intensity: flops per HBM byte (the
@@ -334,11 +348,13 @@ def main():
             "unit": "TFLOP/s",
             "frac": achieved / peak,
             "traffic": traffic,
+            "mfma_busy": load_mfma_busy(bwd_kernel, d, src),
             "algorithmic_flops_per_launch": alg_bwd_launch,
             "avg_launch_ms": bwd_launch_ms,
-            "forward": {"kernel": "fwd_sweep2" if dt_name != "f32" and d % 128 == 0 and d <= 1024 else "fwd_sweep",
+            "forward": {"kernel": fwd_kernel,
                         "achieved": alg_fwd_launch / (fwd_launch_ms * 1e-3) / 1e12,
-                        "frac": alg_fwd_launch / (fwd_launch_ms * 1e-3) / peak, "avg_launch_ms": fwd_launch_ms},
+                        "frac": alg_fwd_launch / (fwd_launch_ms * 1e-3) / peak, "avg_launch_ms": fwd_launch_ms,
+                        "mfma_busy": load_mfma_busy(fwd_kernel, d, source_hash("fwd2.hip", "sweep.hpp", "common.hpp"))},
         },
         "cpu_baseline": None,
         "device": device_info(torch),
