@@ -196,8 +196,9 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
 
-    # the large workloads take seconds to minutes per step: say so on stderr
-    progress = b >= (1 << 17)
+    # the largest workloads take seconds to minutes per step: say so on stderr
+    # (after every forward and backward, so that no silence lasts a whole step)
+    progress = b >= (1 << 20)
     t_start = time.perf_counter()
 
     def note(msg):
@@ -236,6 +237,9 @@ def main():
         infcl.infcl_fwd(img, txt, scale, loss, loss64, lse_r, lse_c, aux, ws)
         if ev is not None:
             ev[1].record()
+        if progress:
+            torch.cuda.synchronize()
+            note("forward done")
         infcl.infcl_bwd(img, txt, scale, lse_r, lse_c, aux, None, dimg, dtxt, dscale, ws)
         if ev is not None:
             ev[2].record()
@@ -266,6 +270,7 @@ def main():
     note(f"inputs resident (b={b}, d={d}); first step")
     step()
     torch.cuda.synchronize()
+    note("first step done")
     peak_bytes = torch.cuda.max_memory_allocated(dev)
     for w in range(a.warmup):
         note(f"warm-up step {w + 1}/{a.warmup}")
