@@ -317,6 +317,14 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
 // that ends iteration t-3, i.e. after the last reads of the tile three places
 // earlier), read by GEMM1 in iteration t-1 and by GEMM2 in iteration t.
 // At d = 1024 three tiles (3 x 64 KiB) do not fit in LDS: bwd_wide serves it.
+// It is also used at d = 768 only while the swept matrix (b d 2 bytes) is at
+// most kPipeSweptBytes: measured against bwd_wide, it is 2.7% faster at
+// 192 MiB of swept rows (b = 131072) and 4.9-5.2% slower at 240 MiB,
+// 384 MiB and 1.5 GiB (b = 163840, 262144, 1048576), where the tile DMA
+// arrives from beyond the 256 MiB last-level cache: bwd_wide's DMA, paced by
+// the G' work it is interleaved with, tolerates that latency; the burst here
+// does not (an L2 prefetch of the tile ahead made it slower still).
+constexpr int64_t kPipeSweptBytes = (int64_t)200 << 20;
 template <int D, bool F16>
 __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
   constexpr int KS = D / 16;
@@ -601,10 +609,17 @@ int bwd_wide_workgroups(int64_t nown) { return (int)((nown + kWideBM - 1) / kWid
 int launch_bwd_wide(const BwdParams& p, int nwg, bool f16, hipStream_t stream) {
   switch (p.d) {
     case 768:
-      if (f16)
-        hipLaunchKernelGGL((bwd_wide3<768, true>), dim3(nwg), dim3(256), 0, stream, p);
-      else
-        hipLaunchKernelGGL((bwd_wide3<768, false>), dim3(nwg), dim3(256), 0, stream, p);
+      if (p.b * 768 * 2 <= kPipeSweptBytes) {
+        if (f16)
+          hipLaunchKernelGGL((bwd_wide3<768, true>), dim3(nwg), dim3(256), 0, stream, p);
+        else
+          hipLaunchKernelGGL((bwd_wide3<768, false>), dim3(nwg), dim3(256), 0, stream, p);
+      } else {
+        if (f16)
+          hipLaunchKernelGGL((bwd_wide<768, true>), dim3(nwg), dim3(256), 0, stream, p);
+        else
+          hipLaunchKernelGGL((bwd_wide<768, false>), dim3(nwg), dim3(256), 0, stream, p);
+      }
       break;
     case 1024:
       if (f16)

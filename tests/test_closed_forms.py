@@ -89,7 +89,8 @@ def _closed_C(b, d, s):
     return loss, r, coef[cls], ds, bound
 
 
-@pytest.mark.parametrize("b,d,s", [(32768, 512, 14.29), (131072, 768, 100.0), (5000, 128, 50.0), (33000, 256, 14.29)])
+@pytest.mark.parametrize("b,d,s", [(32768, 512, 14.29), (131072, 768, 100.0), (163840, 768, 50.0), (5000, 128, 50.0),
+                                   (33000, 256, 14.29)])
 def test_C_periodic_one_hot(b, d, s):
     s32 = f32_scale(s)
     I = _onehot(b, d, d)
