@@ -333,7 +333,10 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
   constexpr int TILEB = kBwdBN * ROWG;
   constexpr int NIW = TILEB / 4096;  // 1 KiB DMA instructions per wave and tile
   constexpr int FBW = D / 128;       // 32-feature blocks of GEMM2 per wave
-  constexpr int kPre = 4;
+#ifndef INFCL_W3_PRE
+#define INFCL_W3_PRE 8
+#endif
+  constexpr int kPre = INFCL_W3_PRE;
   constexpr int NG = 2 * FBW;  // GEMM2 groups
   static_assert(KH % 8 == 0 && KH >= 8, "feature halves start on a 128-feature segment");
   static_assert(3 * TILEB + 3 * 1024 + kWideBM * kBwdBN * 2 + 4 * 64 * 8 * 4 <= 160 * 1024, "LDS budget");
@@ -374,11 +377,37 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
   const float uO = own_ok ? p.udiag[iown] : 0.f;
   const float gdiag = own_ok ? expm1f(-p.ell_own[iown]) + expm1f(-p.ell_swept[iown]) : 0.f;
 
-  auto opaque_lane = [&]() {
-    int lo = lane;
-    asm volatile("" : "+v"(lo));
-    return lo;
-  };
+  // Per-lane address parts, computed once: the kernel has registers to spare
+  // at d = 768, and rebuilding them per tile costs several hundred VALU
+  // cycles in phases without MFMAs.
+  const uint32_t dma_lo = sweep_dma_lane_off(lane, wave, ROWG);
+  const uint32_t lse_lo = 16u * (uint32_t)(lane & 7);
+  int offA[8];  // GEMM1's swept fragments: tile base + kSeg (n >> 3) + offA[n & 7]
+  {
+    const int rA = sweep_perm(l32);
+    const int gA = sweep_g(rA);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) offA[k] = rA * kSegRow + 16 * ((2 * k + h) ^ gA);
+  }
+  int offB[2][FBW];  // GEMM2's transposing reads: tile base + offB + 16 kSegRow s2
+  int offG[2];       // GEMM2's G' fragments of feature step s2
+  {
+    const int g4 = lane >> 4, l16 = lane & 15;
+    const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
+    const int lb = 2 * nb16 + (qq >> 1);
+    const int fo = (qq & 1) * 8;
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int fbw = 0; fbw < FBW; ++fbw) {
+        const int fbabs = wave * FBW + fbw;
+        offB[tt][fbw] = (8 * hh + 4 * tt + e) * kSegRow + kSeg * (fbabs >> 2) +
+                        16 * (4 * ((fbabs & 3) ^ e) + (lb ^ ((tt + 2 * hh) & 3))) + fo;
+      }
+    const int gsw = (l32 >> 2) & 3;
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) offG[s2] = l32 * 64 + 16 * ((2 * s2 + h) ^ gsw);
+  }
   auto tile_rsrc = [&](int jt) {
     const int64_t j0 = (int64_t)(jt < 0 ? 0 : jt) * kBwdBN;
     return rsrc_words((const char*)p.swept + j0 * ROWG, jt < 0 ? 0 : (b - j0) * ROWG);
@@ -393,10 +422,10 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
   // log-sum-exp slot (8 copies of the tile's 32 values, all waves alike)
   auto dma_part = [&](int jt, int kk) {
     if (kk < NIW) {
-      const uint32_t lo = sweep_dma_lane_off(opaque_lane(), wave, ROWG);
-      dma16_asm(tile_rsrc(jt < ntile ? jt : -1), tbuf(jt) + 1024 * (wave + 4 * kk), lo + sweep_dma_kk_off(kk, wave, ROWG));
+      dma16_asm(tile_rsrc(jt < ntile ? jt : -1), tbuf(jt) + 1024 * (wave + 4 * kk),
+                dma_lo + sweep_dma_kk_off(kk, wave, ROWG));
     } else {
-      dma16_asm(lse_rsrc(jt < ntile ? jt : -1), lbuf(jt), 16u * (uint32_t)(opaque_lane() & 7));
+      dma16_asm(lse_rsrc(jt < ntile ? jt : -1), lbuf(jt), lse_lo);
     }
   };
 
@@ -421,14 +450,6 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
   // of tile t1.
   auto stage1 = [&](int t1, const float (&x)[8], const f32x4& L0, const f32x4& L1, float (&gv)[8], float& ds_t,
                     bool with_gp) {
-    int offA[8];
-    {
-      const int lo = opaque_lane();
-      const int rA = sweep_perm(lo & 31);
-      const int gA = sweep_g(rA);
-#pragma unroll
-      for (int k = 0; k < 8; ++k) offA[k] = rA * kSegRow + 16 * ((2 * k + (lo >> 5)) ^ gA);
-    }
     const INFCL_LDS char* half = tbuf(t1) + kSeg * (kh * KH / 8);
     f32x16 sacc;
     bf16x8 ring[kPre];
@@ -446,6 +467,9 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
       if (with_gp && s2 % 3 == 1) {
         const int i = s2 / 3;  // 8 entries over the 24 MFMAs
         gv[i] = gp_entry(x[i], i < 4 ? L0[i] : L1[i - 4], ds_t);
+        // kept here: the compiler would otherwise move part of the entry's
+        // arithmetic past the MFMAs, into the phase after them
+        asm volatile("" : "+v"(gv[i]), "+v"(ds_t));
       }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -456,22 +480,12 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
   // the tile's features, transposing reads two groups ahead)
   auto stage2 = [&](int t) {
     const INFCL_LDS char* cur = tbuf(t);
-    const int lo = opaque_lane();
-    const int l32o = lo & 31, ho = lo >> 5;
-    const int g4 = lo >> 4, l16 = lo & 15;
-    const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
-    const int lb = 2 * nb16 + (qq >> 1);
-    const int fo = (qq & 1) * 8;
-    const int gpo = l32o * 64;
-    const int gsw = (l32o >> 2) & 3;
     auto readB = [&](int g, s16x4 (&bq)[2]) {
-      const int s2 = g / FBW, fbabs = wave * FBW + g % FBW;
+      const int s2 = g / FBW;
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt) {
-        const int off = (8 * hh + 4 * tt + e + 16 * s2) * kSegRow + kSeg * (fbabs >> 2) +
-                        16 * (4 * ((fbabs & 3) ^ e) + (lb ^ ((tt + 2 * hh) & 3))) + fo;
-        bq[tt] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFCL_LDS s16x4*)(cur + off));
-      }
+      for (int tt = 0; tt < 2; ++tt)
+        bq[tt] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (INFCL_LDS s16x4*)(cur + offB[tt][g % FBW] + 16 * kSegRow * s2));
     };
     bf16x8 A[2];
     s16x4 bq[3][2];
@@ -483,7 +497,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
       if (fbw == 0) {
 #pragma unroll
         for (int o2 = 0; o2 < 2; ++o2)
-          A[o2] = *(const INFCL_LDS bf16x8*)(gp + 2048 * o2 + gpo + 16 * ((2 * s2 + ho) ^ gsw));
+          A[o2] = *(const INFCL_LDS bf16x8*)(gp + 2048 * o2 + offG[s2]);
       }
       if (g + 2 < NG) readB(g + 2, bq[(g + 2) % 3]);
       const s16x4* q = bq[g % 3];

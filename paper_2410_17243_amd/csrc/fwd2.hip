@@ -179,7 +179,14 @@ __global__ void __launch_bounds__(64 * fwd2_waves(D), D > 512 ? 1 : 2) fwd_sweep
   constexpr int ROWG = D * 2;
   constexpr int TILEB = kSweepBN * ROWG;
   constexpr int NIW = TILEB / 1024 / NW;  // 1 KiB DMA instructions per wave and tile
-  constexpr int kPre = KS < 4 ? KS : 4;
+#ifndef INFCL_F2_PRE
+#define INFCL_F2_PRE 4
+#endif
+#ifndef INFCL_F2_PRE_WIDE
+#define INFCL_F2_PRE_WIDE 8
+#endif
+  constexpr int kPreD = D > 512 ? INFCL_F2_PRE_WIDE : INFCL_F2_PRE;
+  constexpr int kPre = KS < kPreD ? KS : kPreD;
   static_assert(D % 64 == 0 && D <= 1024 && NIW >= 1 && KS % NIW == 0, "tile DMA layout");
   static_assert((D > 512 ? 1 : 2) * (2 * TILEB + 4 * 1024 + 5 * 512) <= 160 * 1024, "workgroups per CU");
   __shared__ __attribute__((aligned(1024))) char tA_[TILEB];
@@ -216,11 +223,19 @@ __global__ void __launch_bounds__(64 * fwd2_waves(D), D > 512 ? 1 : 2) fwd_sweep
   float* const cR = p.colR + (int64_t)q * b;
   float* const cL = p.colL + (int64_t)q * b;
 
-  auto opaque_lane = [&]() {
-    int lo = lane;
-    asm volatile("" : "+v"(lo));
-    return lo;
-  };
+  // Per-lane address parts, computed once (rebuilding them per tile costs
+  // VALU cycles between the tile's phases): the DMA source offset of this
+  // lane, the column-pair slot offset, and GEMM1's swept fragment offsets
+  // (tile base + kSeg (n >> 3) + offA[n & 7]).
+  const uint32_t dma_lo = sweep_dma_lane_off(lane, wq, ROWG);
+  const uint32_t slot_lo = 16u * (uint32_t)(lane & 7);
+  int offA[8];
+  {
+    const int rA = sweep_perm(l32);
+    const int gA = sweep_g(rA);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) offA[k] = rA * kSegRow + 16 * ((2 * k + h) ^ gA);
+  }
   // swept row (tile-relative) of accumulator entry r of this lane
   auto jrow = [&](int r) { return 16 * (r >> 3) + 8 * h + (r & 7); };
   auto tile_rsrc = [&](int jt) {
@@ -233,9 +248,8 @@ __global__ void __launch_bounds__(64 * fwd2_waves(D), D > 512 ? 1 : 2) fwd_sweep
   auto issue_slot = [&](int jt, bool first_rb, INFCL_LDS float* slot) {
     const int j0 = (jt < 0 ? 0 : jt) * kSweepBN;
     const int64_t nb = jt < 0 ? 0 : (int64_t)(b - j0) * 4;
-    const uint32_t so = 16u * (uint32_t)(opaque_lane() & 7);
-    dma16_asm(rsrc_words(first_rb ? p.ref2 + j0 : cR + j0, nb), slot, so);
-    dma16_asm(rsrc_words(cL + j0, first_rb ? 0 : nb), slot + 256, so);
+    dma16_asm(rsrc_words(first_rb ? p.ref2 + j0 : cR + j0, nb), slot, slot_lo);
+    dma16_asm(rsrc_words(cL + j0, first_rb ? 0 : nb), slot + 256, slot_lo);
   };
 
   for (int rb = q; rb < p.nRB; rb += p.Pr) {
@@ -269,10 +283,9 @@ __global__ void __launch_bounds__(64 * fwd2_waves(D), D > 512 ? 1 : 2) fwd_sweep
 
     {
       const u32x4 rs = tile_rsrc(ct_lo);
-      const uint32_t lo = sweep_dma_lane_off(opaque_lane(), wq, ROWG);
 #pragma unroll
       for (int k = 0; k < NIW; ++k)
-        dma16_asm(rs, tA + 1024 * (wq + 4 * (kk0 + k)), lo + sweep_dma_kk_off(kk0 + k, wq, ROWG));
+        dma16_asm(rs, tA + 1024 * (wq + 4 * (kk0 + k)), dma_lo + sweep_dma_kk_off(kk0 + k, wq, ROWG));
       if (slot_wave) issue_slot(ct_lo, first_rb, sA);
     }
     wait_dma();
@@ -350,16 +363,7 @@ __global__ void __launch_bounds__(64 * fwd2_waves(D), D > 512 ? 1 : 2) fwd_sweep
       pairs(par ^ 1, prw, psw);
       f32x16 sacc;
       {
-        int offA[8];
-        {
-          const int lo = opaque_lane();
-          const int rA = sweep_perm(lo & 31);
-          const int gA = sweep_g(rA);
-#pragma unroll
-          for (int k = 0; k < 8; ++k) offA[k] = rA * kSegRow + 16 * ((2 * k + (lo >> 5)) ^ gA);
-        }
         const u32x4 drs = tile_rsrc(jn);
-        const uint32_t dlo = sweep_dma_lane_off(opaque_lane(), wq, ROWG);
         bf16x8 ring[kPre];
 #pragma unroll
         for (int i = 0; i < kPre; ++i) ring[i] = *(const INFCL_LDS bf16x8*)(cur + offA[i & 7] + kSeg * (i >> 3));
@@ -373,7 +377,7 @@ __global__ void __launch_bounds__(64 * fwd2_waves(D), D > 512 ? 1 : 2) fwd_sweep
           constexpr int SPI = KS / NIW;  // steps per DMA instruction
           if ((s2 + 1) % SPI == 0) {
             const int kk = kk0 + (s2 + 1) / SPI - 1;
-            dma16_asm(drs, nxt + 1024 * (wq + 4 * kk), dlo + sweep_dma_kk_off(kk, wq, ROWG));
+            dma16_asm(drs, nxt + 1024 * (wq + 4 * kk), dma_lo + sweep_dma_kk_off(kk, wq, ROWG));
           }
           if (slot_wave && s2 == (KS > 1 ? 1 : 0)) issue_slot(jn, first_rb, snxt);
           if (s2 + kPre < KS) {
