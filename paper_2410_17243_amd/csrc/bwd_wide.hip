@@ -103,6 +103,44 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
     return rsrc_words(p.lse2_swept + j0, jt < 0 ? 0 : (b - j0) * 4);
   };
   auto lse_lane_off = [&]() { return 16u * (uint32_t)(opaque_lane() & 7); };
+  // Per-lane address parts.  Where registers allow (d <= 768) they are
+  // computed once; at d = 1024 all 512 registers are taken and they are
+  // rebuilt at each use from an opaque lane id instead (a value held across
+  // the loop would be spilled, and a scratch reload waits for all DMA in
+  // flight).
+  constexpr bool kHoist = D <= 768;
+  const uint32_t dma_lo_h = sweep_dma_lane_off(lane, wave, ROWG);
+  auto dma_lo = [&]() { return kHoist ? dma_lo_h : sweep_dma_lane_off(opaque_lane(), wave, ROWG); };
+  auto make_offA = [&](int lo, int (&o)[8]) {
+    const int rA = sweep_perm(lo & 31);
+    const int gA = sweep_g(rA);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) o[k] = rA * kSegRow + 16 * ((2 * k + (lo >> 5)) ^ gA);
+  };
+  // GEMM2's transposing reads (tile base + offB[t][fbw] + 16 kSegRow s2) and
+  // G' fragments (G' block + offG[s2])
+  auto make_offBG = [&](int lo, int (&oB)[2][FBW], int (&oG)[2]) {
+    const int g4 = lo >> 4, l16 = lo & 15;
+    const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
+    const int lb = 2 * nb16 + (qq >> 1);
+    const int fo = (qq & 1) * 8;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int fbw = 0; fbw < FBW; ++fbw) {
+        const int fbabs = wave * FBW + fbw;
+        oB[t][fbw] = (8 * hh + 4 * t + e) * kSegRow + kSeg * (fbabs >> 2) +
+                     16 * (4 * ((fbabs & 3) ^ e) + (lb ^ ((t + 2 * hh) & 3))) + fo;
+      }
+    const int l32o = lo & 31, gsw = (l32o >> 2) & 3;
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) oG[s2] = l32o * 64 + 16 * ((2 * s2 + (lo >> 5)) ^ gsw);
+  };
+  int offA_h[8], offB_h[2][FBW], offG_h[2];
+  if constexpr (kHoist) {
+    make_offA(lane, offA_h);
+    make_offBG(lane, offB_h, offG_h);
+  }
 
   double ds_acc = 0.0;
   f32x16 dacc[2 * FBW];
@@ -115,12 +153,11 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
   // DMA of tile dtile's log-sum-exp slot
   auto gemm1 = [&](const INFCL_LDS char* cur, int dtile, INFCL_LDS float* dlse) {
     int offA[8];
-    {
-      const int lo = opaque_lane();
-      const int rA = sweep_perm(lo & 31);
-      const int gA = sweep_g(rA);
+    if constexpr (kHoist) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k) offA[k] = rA * kSegRow + 16 * ((2 * k + (lo >> 5)) ^ gA);
+      for (int k = 0; k < 8; ++k) offA[k] = offA_h[k];
+    } else {
+      make_offA(opaque_lane(), offA);
     }
     const INFCL_LDS char* half = cur + kSeg * (kh * KH / 8);
     const u32x4 drl = lse_rsrc(dtile);
@@ -166,7 +203,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
     float ds_tile = 0.f;
     bf16x8 ga;
     const u32x4 drs = tile_rsrc(dtile);
-    const uint32_t dlo = sweep_dma_lane_off(opaque_lane(), wave, ROWG);
+    const uint32_t dlo = dma_lo();
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
 #pragma unroll
@@ -198,22 +235,23 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
   // ---- GEMM2: all 64 own rows' G' x this wave's quarter of the tile's
   // features (transposing reads of the segment-blocked tile)
   auto gemm2 = [&](const INFCL_LDS char* cur) {
-    const int lo = opaque_lane();
-    const int l32o = lo & 31, ho = lo >> 5;
-    const int g4 = lo >> 4, l16 = lo & 15;
-    const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
-    const int lb = 2 * nb16 + (qq >> 1);
-    const int fo = (qq & 1) * 8;
-    const int gpo = l32o * 64;
-    const int gsw = (l32o >> 2) & 3;
-    auto readB = [&](int g, s16x4 (&bq)[2]) {
-      const int s2 = g / FBW, fbabs = wave * FBW + g % FBW;
+    int offB[2][FBW], offG[2];
+    if constexpr (kHoist) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const int off = (8 * hh + 4 * t + e + 16 * s2) * kSegRow + kSeg * (fbabs >> 2) +
-                        16 * (4 * ((fbabs & 3) ^ e) + (lb ^ ((t + 2 * hh) & 3))) + fo;
-        bq[t] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFCL_LDS s16x4*)(cur + off));
-      }
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int fbw = 0; fbw < FBW; ++fbw) offB[t][fbw] = offB_h[t][fbw];
+      offG[0] = offG_h[0];
+      offG[1] = offG_h[1];
+    } else {
+      make_offBG(opaque_lane(), offB, offG);
+    }
+    auto readB = [&](int g, s16x4 (&bq)[2]) {
+      const int s2 = g / FBW;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+        bq[t] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (INFCL_LDS s16x4*)(cur + offB[t][g % FBW] + 16 * kSegRow * s2));
     };
     // one group (contraction half s2, feature block fbw) per stage, the
     // transposing reads two stages ahead; stages are separate scheduling
@@ -228,7 +266,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
       if (fbw == 0) {
 #pragma unroll
         for (int o2 = 0; o2 < 2; ++o2)
-          A[o2] = *(const INFCL_LDS bf16x8*)(gp + 2048 * o2 + gpo + 16 * ((2 * s2 + ho) ^ gsw));
+          A[o2] = *(const INFCL_LDS bf16x8*)(gp + 2048 * o2 + offG[s2]);
       }
       if (g + 2 < 2 * FBW) readB(g + 2, bq[(g + 2) % 3]);
       const s16x4* q = bq[g % 3];
@@ -254,7 +292,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
   };
   {
     const u32x4 rs = tile_rsrc(0);
-    const uint32_t lo = sweep_dma_lane_off(opaque_lane(), wave, ROWG);
+    const uint32_t lo = dma_lo();
 #pragma unroll
     for (int kk = 0; kk < NIW; ++kk) dma16_asm(rs, tA + 1024 * (wave + 4 * kk), lo + sweep_dma_kk_off(kk, wave, ROWG));
     dma16_asm(lse_rsrc(0), lA, lse_lane_off());
@@ -324,7 +362,10 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
 // arrives from beyond the 256 MiB last-level cache: bwd_wide's DMA, paced by
 // the G' work it is interleaved with, tolerates that latency; the burst here
 // does not (an L2 prefetch of the tile ahead made it slower still).
-constexpr int64_t kPipeSweptBytes = (int64_t)200 << 20;
+#ifndef INFCL_PIPE_SWEPT_MIB
+#define INFCL_PIPE_SWEPT_MIB 200
+#endif
+constexpr int64_t kPipeSweptBytes = (int64_t)INFCL_PIPE_SWEPT_MIB << 20;
 template <int D, bool F16>
 __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
   constexpr int KS = D / 16;
