@@ -111,8 +111,12 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
   constexpr bool kHoist = D <= 768;
   const uint32_t dma_lo_h = sweep_dma_lane_off(lane, wave, ROWG);
   auto dma_lo = [&]() { return kHoist ? dma_lo_h : sweep_dma_lane_off(opaque_lane(), wave, ROWG); };
+  // The kh = 1 wave loads the tile's rows 16..31 into MFMA rows 0..15 and
+  // rows 0..15 into 16..31 (row index XOR 16; the row does not enter the bank
+  // of a chunk): accumulator entries 0..7 of either wave are then the ones it
+  // finishes (tile rows 16 kh + 8 h + i), entries 8..15 the ones it hands over.
   auto make_offA = [&](int lo, int (&o)[8]) {
-    const int rA = sweep_perm(lo & 31);
+    const int rA = sweep_perm(lo & 31) ^ (16 * kh);
     const int gA = sweep_g(rA);
 #pragma unroll
     for (int k = 0; k < 8; ++k) o[k] = rA * kSegRow + 16 * ((2 * k + (lo >> 5)) ^ gA);
@@ -179,7 +183,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
     return sacc;
   };
 
-  // ---- join, G' of the wave's 8 entries (entry r = 8 kh + i <-> swept row
+  // ---- join, G' of the wave's 8 entries (entry i <-> swept row
   // 16 kh + 8h + i of the tile) into the G' block, with the DMA of tile
   // dtile into ddst spread over the entries; returns dscale's share
   auto join_gp = [&](int jt, const INFCL_LDS float* lcur, const f32x16& sacc, int dtile,
@@ -187,8 +191,8 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
     float mine[8], other[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      mine[i] = kh ? sacc[8 + i] : sacc[i];
-      other[i] = kh ? sacc[i] : sacc[8 + i];
+      mine[i] = sacc[i];
+      other[i] = sacc[8 + i];
     }
     *(INFCL_LDS f32x4*)&xs_[wave][lane][0] = f32x4{other[0], other[1], other[2], other[3]};
     *(INFCL_LDS f32x4*)&xs_[wave][lane][4] = f32x4{other[4], other[5], other[6], other[7]};
@@ -423,9 +427,15 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
   // cycles in phases without MFMAs.
   const uint32_t dma_lo = sweep_dma_lane_off(lane, wave, ROWG);
   const uint32_t lse_lo = 16u * (uint32_t)(lane & 7);
-  int offA[8];  // GEMM1's swept fragments: tile base + kSeg (n >> 3) + offA[n & 7]
+  // GEMM1's swept fragments: tile base + kSeg (n >> 3) + offA[n & 7].  The
+  // kh = 1 wave loads the tile's rows 16..31 into MFMA rows 0..15 and rows
+  // 0..15 into 16..31 (row index XOR 16; the row does not enter the bank of
+  // a chunk, so the reads stay conflict free): then accumulator entries 0..7
+  // of either wave are the ones it finishes (tile rows 16 kh + 8 h + i) and
+  // entries 8..15 the ones it hands over, with no selection by kh.
+  int offA[8];
   {
-    const int rA = sweep_perm(l32);
+    const int rA = sweep_perm(l32) ^ (16 * kh);
     const int gA = sweep_g(rA);
 #pragma unroll
     for (int k = 0; k < 8; ++k) offA[k] = rA * kSegRow + 16 * ((2 * k + h) ^ gA);
@@ -565,11 +575,9 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
     const f32x16 sacc = stage1(0, x0, z, z, gv0, ds0, false);
     float mine[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) mine[i] = kh ? sacc[8 + i] : sacc[i];
-    *(INFCL_LDS f32x4*)&xs_[wave][lane][0] = f32x4{kh ? sacc[0] : sacc[8], kh ? sacc[1] : sacc[9],
-                                                   kh ? sacc[2] : sacc[10], kh ? sacc[3] : sacc[11]};
-    *(INFCL_LDS f32x4*)&xs_[wave][lane][4] = f32x4{kh ? sacc[4] : sacc[12], kh ? sacc[5] : sacc[13],
-                                                   kh ? sacc[6] : sacc[14], kh ? sacc[7] : sacc[15]};
+    for (int i = 0; i < 8; ++i) mine[i] = sacc[i];
+    *(INFCL_LDS f32x4*)&xs_[wave][lane][0] = f32x4{sacc[8], sacc[9], sacc[10], sacc[11]};
+    *(INFCL_LDS f32x4*)&xs_[wave][lane][4] = f32x4{sacc[12], sacc[13], sacc[14], sacc[15]};
     __syncthreads();
     const f32x4 q0 = *(const INFCL_LDS f32x4*)&xs_[wave ^ 1][lane][0];
     const f32x4 q1 = *(const INFCL_LDS f32x4*)&xs_[wave ^ 1][lane][4];
@@ -611,11 +619,9 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
       const int row = 32 * ob + l32;
       *(INFCL_LDS bf16x8*)(gp + row * 64 + 16 * ((2 * kh + h) ^ ((row >> 2) & 3))) = ga;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) mine[i] = kh ? sacc[8 + i] : sacc[i];
-      *(INFCL_LDS f32x4*)&xs_[wave][lane][0] = f32x4{kh ? sacc[0] : sacc[8], kh ? sacc[1] : sacc[9],
-                                                     kh ? sacc[2] : sacc[10], kh ? sacc[3] : sacc[11]};
-      *(INFCL_LDS f32x4*)&xs_[wave][lane][4] = f32x4{kh ? sacc[4] : sacc[12], kh ? sacc[5] : sacc[13],
-                                                     kh ? sacc[6] : sacc[14], kh ? sacc[7] : sacc[15]};
+      for (int i = 0; i < 8; ++i) mine[i] = sacc[i];
+      *(INFCL_LDS f32x4*)&xs_[wave][lane][0] = f32x4{sacc[8], sacc[9], sacc[10], sacc[11]};
+      *(INFCL_LDS f32x4*)&xs_[wave][lane][4] = f32x4{sacc[12], sacc[13], sacc[14], sacc[15]};
 #pragma unroll
       for (int kk = 0; kk <= NIW; ++kk) dma_part(t + 2, kk);
     }
