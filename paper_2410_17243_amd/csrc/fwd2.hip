@@ -41,9 +41,22 @@
 //  the sweep makes no other loads, and (as in the backward sweep) the DMA is
 //  issued from inline assembly, so the compiler never waits for it before
 //  unrelated LDS reads.
+#include <utility>
+
 #include "sweep.hpp"
 
 namespace infcl {
+
+// f(std::integral_constant<int, 0>), ..., f(std::integral_constant<int, N-1>):
+// a loop unrolled by construction, with a compile-time index in each body.
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 struct Fwd2Params {
   const __bf16* img;  // own rows i, [b, d] (bf16, or fp16 bits)
@@ -348,46 +361,41 @@ __global__ void __launch_bounds__(64 * fwd2_waves(D), D > 512 ? 1 : 2) fwd_sweep
       }
     };
 
-    // one tile: GEMM1 of the tile in cur (issuing the DMA of tile jt+1 into
-    // nxt between its MFMAs), the pending merge, row statistics, column
-    // partial pairs into LDS
-    auto body = [&](int jt, const INFCL_LDS char* cur, const INFCL_LDS float* scur, INFCL_LDS char* nxt,
-                    INFCL_LDS float* snxt, int par) {
-      const int j0 = jt * kSweepBN;
-      const int jn = jt + 1 < ct_hi ? jt + 1 : -1;
-      const int ci = rs16_index(lane);
-      const int jl = jrow(ci);  // the column whose partial this lane ends with
-      const float Rmine = scur[jl], Lmine = scur[256 + jl];
-      const float Rold = scur[jc], Lold = scur[256 + jc];
-      float prw[NW], psw[NW];
-      pairs(par ^ 1, prw, psw);
+    // GEMM1 of the tile in cur (S^T block of the wave's rows), with the DMA
+    // of tile jn into nxt (its column pairs into snxt) issued between the MFMAs
+    auto gemm1 = [&](const INFCL_LDS char* cur, int jn, INFCL_LDS char* nxt, INFCL_LDS float* snxt) {
       f32x16 sacc;
-      {
-        const u32x4 drs = tile_rsrc(jn);
-        bf16x8 ring[kPre];
+      const u32x4 drs = tile_rsrc(jn);
+      bf16x8 ring[kPre];
 #pragma unroll
-        for (int i = 0; i < kPre; ++i) ring[i] = *(const INFCL_LDS bf16x8*)(cur + offA[i & 7] + kSeg * (i >> 3));
-        __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
-#pragma unroll
-        for (int s2 = 0; s2 < KS; ++s2) {
-          if constexpr (D > 512)  // own rows in AGPRs
-            mfma16_vgpr_ab<F16>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KS - 1);
-          else
-            mfma16_vgpr<F16>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KS - 1);
-          constexpr int SPI = KS / NIW;  // steps per DMA instruction
-          if ((s2 + 1) % SPI == 0) {
-            const int kk = kk0 + (s2 + 1) / SPI - 1;
-            dma16_asm(drs, nxt + 1024 * (wq + 4 * kk), dma_lo + sweep_dma_kk_off(kk, wq, ROWG));
-          }
-          if (slot_wave && s2 == (KS > 1 ? 1 : 0)) issue_slot(jn, first_rb, snxt);
-          if (s2 + kPre < KS) {
-            const int n = s2 + kPre;
-            ring[s2 % kPre] = *(const INFCL_LDS bf16x8*)(cur + offA[n & 7] + kSeg * (n >> 3));
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-          }
+      for (int i = 0; i < kPre; ++i) ring[i] = *(const INFCL_LDS bf16x8*)(cur + offA[i & 7] + kSeg * (i >> 3));
+      __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
+      static_for<KS>([&](auto s2c) {
+        constexpr int s2 = decltype(s2c)::value;
+        if constexpr (D > 512)  // own rows in AGPRs
+          mfma16_vgpr_ab<F16>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KS - 1);
+        else
+          mfma16_vgpr<F16>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KS - 1);
+        constexpr int SPI = KS / NIW;  // steps per DMA instruction
+        if ((s2 + 1) % SPI == 0) {
+          const int kk = kk0 + (s2 + 1) / SPI - 1;
+          dma16_asm(drs, nxt + 1024 * (wq + 4 * kk), dma_lo + sweep_dma_kk_off(kk, wq, ROWG));
         }
-      }
-      merge(prw, psw);
+        if (slot_wave && s2 == (KS > 1 ? 1 : 0)) issue_slot(jn, first_rb, snxt);
+        if constexpr (s2 + kPre < KS) {
+          constexpr int n = s2 + kPre;
+          ring[s2 % kPre] = *(const INFCL_LDS bf16x8*)(cur + offA[n & 7] + kSeg * (n >> 3));
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+      });
+      return sacc;
+    };
+
+    // Statistics of tile jt from its S^T block: row update, this wave's column
+    // partial pairs into LDS (parity par)
+    auto stats = [&](int jt, const f32x16& sacc, const INFCL_LDS float* scur, int par, float Rmine, float Lmine) {
+      const int j0 = jt * kSweepBN;
+      const int jl = jrow(rs16_index(lane));  // the column whose partial this lane ends with
       // entries off the problem or on the diagonal take no part (uniform test)
       const bool special = (j0 == own0) || (j0 + kSweepBN > b) || !wave_rows_ok;
       // (bitwise operators: no short-circuit branches)
@@ -395,8 +403,14 @@ __global__ void __launch_bounds__(64 * fwd2_waves(D), D > 512 ? 1 : 2) fwd_sweep
         const int j = j0 + jrow(r);
         return (bool)(own_ok & (j < b) & (j != iown));
       };
-      // scaled entry r, -inf when it takes no part
-      auto yv = [&](int r) { return (!special | keep(r)) ? sacc[r] * k2 : ninf; };
+      // scaled entry r, -inf when it takes no part.  Used only on the rare
+      // paths below; the opaque copy keeps the compiler from hoisting these
+      // 16 products (and the masks) out of those paths into the common one.
+      auto yv = [&](int r) {
+        float x = sacc[r];
+        asm volatile("" : "+v"(x));
+        return (!special | keep(r)) ? x * k2 : ninf;
+      };
       // ---- row: lazy against its reference, exact when a bound fails
       float e[16];
 #pragma unroll
@@ -474,7 +488,23 @@ __global__ void __launch_bounds__(64 * fwd2_waves(D), D > 512 ? 1 : 2) fwd_sweep
         cxS_[par][jl][wave] = part;
       }
       if (wave_any(rchg)) refresh();
-      pjg = j0 + jc;
+    };
+
+    const int jl_lane = jrow(rs16_index(lane));
+    // one tile: GEMM1 of the tile in cur (issuing the DMA of tile jt+1 into
+    // nxt between its MFMAs), the pending merge, row statistics, column
+    // partial pairs into LDS
+    auto body = [&](int jt, const INFCL_LDS char* cur, const INFCL_LDS float* scur, INFCL_LDS char* nxt,
+                    INFCL_LDS float* snxt, int par) {
+      const int jn = jt + 1 < ct_hi ? jt + 1 : -1;
+      const float Rmine = scur[jl_lane], Lmine = scur[256 + jl_lane];
+      const float Rold = scur[jc], Lold = scur[256 + jc];
+      float prw[NW], psw[NW];
+      pairs(par ^ 1, prw, psw);
+      const f32x16 sacc = gemm1(cur, jn, nxt, snxt);
+      merge(prw, psw);
+      stats(jt, sacc, scur, par, Rmine, Lmine);
+      pjg = jt * kSweepBN + jc;
       pRold = Rold;
       pLold = Lold;
       wait_dma();  // the next tile and its column pairs are in LDS after the barrier
