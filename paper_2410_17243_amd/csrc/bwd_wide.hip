@@ -357,7 +357,9 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
 //            area are free).
 // A tile's buffer is written by its DMA in iteration t-2 (after the barrier
 // that ends iteration t-3, i.e. after the last reads of the tile three places
-// earlier), read by GEMM1 in iteration t-1 and by GEMM2 in iteration t.
+// earlier), read by GEMM1 in iteration t-1 and by GEMM2 in iteration t.  The
+// swept log-sum-exp values a lane needs for tile t are loaded into registers
+// in iteration t-1.
 // At d = 1024 three tiles (3 x 64 KiB) do not fit in LDS: bwd_wide serves it.
 // It is also used at d = 768 only while the swept matrix (b d 2 bytes) is at
 // most kPipeSweptBytes: measured against bwd_wide, it is 2.7% faster at
@@ -384,13 +386,11 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
   constexpr int kPre = INFCL_W3_PRE;
   constexpr int NG = 2 * FBW;  // GEMM2 groups
   static_assert(KH % 8 == 0 && KH >= 8, "feature halves start on a 128-feature segment");
-  static_assert(3 * TILEB + 3 * 1024 + kWideBM * kBwdBN * 2 + 4 * 64 * 8 * 4 <= 160 * 1024, "LDS budget");
+  static_assert(3 * TILEB + kWideBM * kBwdBN * 2 + 4 * 64 * 8 * 4 <= 160 * 1024, "LDS budget");
   __shared__ __attribute__((aligned(1024))) char tiles_[3 * TILEB];
-  __shared__ __attribute__((aligned(1024))) float lses_[3 * 256];
   __shared__ __attribute__((aligned(1024))) char gp_[kWideBM * kBwdBN * 2];
   __shared__ __attribute__((aligned(16))) float xs_[4][64][8];
   INFCL_LDS char* const tiles = (INFCL_LDS char*)tiles_;
-  INFCL_LDS float* const lses = (INFCL_LDS float*)lses_;
   INFCL_LDS char* const gp = (INFCL_LDS char*)gp_;
 
   const int lane = __lane_id();
@@ -426,7 +426,6 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
   // at d = 768, and rebuilding them per tile costs several hundred VALU
   // cycles in phases without MFMAs.
   const uint32_t dma_lo = sweep_dma_lane_off(lane, wave, ROWG);
-  const uint32_t lse_lo = 16u * (uint32_t)(lane & 7);
   // GEMM1's swept fragments: tile base + kSeg (n >> 3) + offA[n & 7].  The
   // kh = 1 wave loads the tile's rows 16..31 into MFMA rows 0..15 and rows
   // 0..15 into 16..31 (row index XOR 16; the row does not enter the bank of
@@ -463,21 +462,25 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
     const int64_t j0 = (int64_t)(jt < 0 ? 0 : jt) * kBwdBN;
     return rsrc_words((const char*)p.swept + j0 * ROWG, jt < 0 ? 0 : (b - j0) * ROWG);
   };
-  auto lse_rsrc = [&](int jt) {
-    const int64_t j0 = (int64_t)(jt < 0 ? 0 : jt) * kBwdBN;
-    return rsrc_words(p.lse2_swept + j0, jt < 0 ? 0 : (b - j0) * 4);
-  };
   auto tbuf = [&](int t) { return tiles + TILEB * (t % 3); };
-  auto lbuf = [&](int t) { return lses + 256 * (t % 3); };
-  // DMA instruction kk of tile jt into its buffer; kk == NIW is the
-  // log-sum-exp slot (8 copies of the tile's 32 values, all waves alike)
+  // DMA instruction kk of tile jt into its buffer
   auto dma_part = [&](int jt, int kk) {
-    if (kk < NIW) {
-      dma16_asm(tile_rsrc(jt < ntile ? jt : -1), tbuf(jt) + 1024 * (wave + 4 * kk),
-                dma_lo + sweep_dma_kk_off(kk, wave, ROWG));
-    } else {
-      dma16_asm(lse_rsrc(jt < ntile ? jt : -1), lbuf(jt), lse_lo);
-    }
+    dma16_asm(tile_rsrc(jt < ntile ? jt : -1), tbuf(jt) + 1024 * (wave + 4 * kk),
+              dma_lo + sweep_dma_kk_off(kk, wave, ROWG));
+  };
+  // The log-sum-exp values of the 8 swept rows 16 kh + 8 h + i of tile jt
+  // whose G' entries the lane forms go straight into registers, one tile
+  // ahead (range-checked buffer loads: zeros past b).  Through an LDS slot
+  // that every wave filled by DMA the backward took 1% longer.
+  auto load_L = [&](int jt, f32x4& A, f32x4& B) {
+    const int64_t j0 = (int64_t)jt * kBwdBN;
+    const bool in = jt < ntile;
+    const int64_t rem = in ? (b - j0) * 4 : 0;
+    const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(p.lse2_swept + (in ? j0 : 0)), (short)0, (int)(rem < 128 ? rem : 128), 0x00020000);
+    const int vo = 4 * (16 * kh + 8 * h);
+    A = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, vo, 0, 0));
+    B = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, vo + 16, 0, 0));
   };
 
   double ds_acc = 0.0;
@@ -564,9 +567,9 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
   float x[8];
   {
 #pragma unroll
-    for (int kk = 0; kk <= NIW; ++kk) dma_part(0, kk);
+    for (int kk = 0; kk < NIW; ++kk) dma_part(0, kk);
 #pragma unroll
-    for (int kk = 0; kk <= NIW; ++kk) dma_part(1, kk);
+    for (int kk = 0; kk < NIW; ++kk) dma_part(1, kk);
     wait_dma();
     __syncthreads();
     float gv0[8], ds0 = 0.f;
@@ -586,13 +589,14 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
     __syncthreads();
   }
 
+  f32x4 Lc0, Lc1, Ln0, Ln1;  // log-sum-exp values of tiles t and t+1
+  load_L(0, Lc0, Lc1);
   for (int t = 0; t < ntile; ++t) {
+    load_L(t + 1, Ln0, Ln1);
     // ---- stage 1
     float mine[8];
     {
-      const INFCL_LDS float* lp = lbuf(t) + 16 * kh + 8 * h;
-      const f32x4 L0 = *(const INFCL_LDS f32x4*)lp;
-      const f32x4 L1 = *(const INFCL_LDS f32x4*)(lp + 4);
+      const f32x4 L0 = Lc0, L1 = Lc1;
       float gv[8], ds_t = 0.f;
       const f32x16 sacc = stage1(t + 1, x, L0, L1, gv, ds_t, true);
       const int64_t j0 = (int64_t)t * kBwdBN;
@@ -623,7 +627,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
       *(INFCL_LDS f32x4*)&xs_[wave][lane][0] = f32x4{sacc[8], sacc[9], sacc[10], sacc[11]};
       *(INFCL_LDS f32x4*)&xs_[wave][lane][4] = f32x4{sacc[12], sacc[13], sacc[14], sacc[15]};
 #pragma unroll
-      for (int kk = 0; kk <= NIW; ++kk) dma_part(t + 2, kk);
+      for (int kk = 0; kk < NIW; ++kk) dma_part(t + 2, kk);
     }
     __syncthreads();  // G' block of tile t complete; join data of tile t+1 visible
     // ---- stage 2
@@ -636,6 +640,8 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
     }
     wait_dma();
     __syncthreads();  // tile t+2 landed; tile t's buffer, the G' block and the join area are free
+    Lc0 = Ln0;
+    Lc1 = Ln1;
   }
 
   // ---- write dOwn (as bwd_wide)
