@@ -194,10 +194,15 @@ def backward(I, T, s, fwd: dict, dloss: float = 1.0, threads: int | None = None)
     dI = np.zeros((b, d))
     dT = np.zeros((b, d))
     ds_parts = []
-    for (r0, r1), (dI_blk, dT_part, ds_part) in zip(blocks, _pmap(blk_grad, blocks, threads)):
-        dI[r0:r1] = dI_blk
-        dT += dT_part
-        ds_parts.append(ds_part)
+    # blocks in groups of `threads`, each group's results added in block order
+    # before the next group starts: a block's dT part is a whole [b, d] array,
+    # so holding every block's part at once would need (b / rows) b d 8 bytes
+    for g0 in range(0, len(blocks), threads):
+        group = blocks[g0:g0 + threads]
+        for (r0, r1), (dI_blk, dT_part, ds_part) in zip(group, _pmap(blk_grad, group, threads)):
+            dI[r0:r1] = dI_blk
+            dT += dT_part
+            ds_parts.append(ds_part)
     dscale = dloss * math.fsum(ds_parts) / (2.0 * b)
     return dI, dT, dscale
 
