@@ -71,6 +71,7 @@ def _grad_rows(A, B, s, rows, lse_own, lse_other, ell_own, ell_other, b):
     return k * (g @ B)
 
 
+@pytest.mark.skipif(not os.path.exists(GOLDEN), reason="stored oracle results absent: run tests/golden/make_c3_reference.py")
 def test_stored_oracle_b131072_d768_s100():
     ref = np.load(GOLDEN, allow_pickle=False)
     c = synth.WORKLOADS[3]
