@@ -1,5 +1,6 @@
 // Backward sweep for wide rows (16-bit inputs: bf16 or fp16, d = 768 or
-// 1024) in a single pass (gfx950).
+// 1024) in a single pass (gfx950): bwd_wide below, the serial form, serves
+// d = 1024; bwd_wide3 further down, the pipelined form, serves d = 768.
 //
 // Same quantities as the 128-row sweep (Sec. 3.1, Eq. 6-8 completed for both
 // halves of the loss and the scale; the appendix's in-GPU backward recomputes
@@ -20,7 +21,8 @@
 //           the next tile (all four waves) is issued here, between the
 //           entries: in this phase, which has no MFMAs, its instructions cost
 //           far less than between GEMM1's MFMAs (a whole-tile phase trace at
-//           d = 768: GEMM1 took 3170 cycles with the DMA and 1300 without);
+//           d = 768, when this form served it: GEMM1 took 3170 cycles with
+//           the DMA and 1300 without);
 //   GEMM2   each wave multiplies all 64 own rows' G' by its quarter of the
 //           features of the tile (transposing LDS reads), accumulating in
 //           AGPRs.
@@ -103,14 +105,10 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
     return rsrc_words(p.lse2_swept + j0, jt < 0 ? 0 : (b - j0) * 4);
   };
   auto lse_lane_off = [&]() { return 16u * (uint32_t)(opaque_lane() & 7); };
-  // Per-lane address parts.  Where registers allow (d <= 768) they are
-  // computed once; at d = 1024 all 512 registers are taken and they are
-  // rebuilt at each use from an opaque lane id instead (a value held across
-  // the loop would be spilled, and a scratch reload waits for all DMA in
-  // flight).
-  constexpr bool kHoist = D <= 768;
-  const uint32_t dma_lo_h = sweep_dma_lane_off(lane, wave, ROWG);
-  auto dma_lo = [&]() { return kHoist ? dma_lo_h : sweep_dma_lane_off(opaque_lane(), wave, ROWG); };
+  // Per-lane address parts are rebuilt at each use from an opaque lane id:
+  // at d = 1024 all 512 registers are taken, so a value held across the loop
+  // would be spilled, and a scratch reload waits for all DMA in flight.
+  auto dma_lo = [&]() { return sweep_dma_lane_off(opaque_lane(), wave, ROWG); };
   // The kh = 1 wave loads the tile's rows 16..31 into MFMA rows 0..15 and
   // rows 0..15 into 16..31 (row index XOR 16; the row does not enter the bank
   // of a chunk): accumulator entries 0..7 of either wave are then the ones it
@@ -140,11 +138,6 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) oG[s2] = l32o * 64 + 16 * ((2 * s2 + (lo >> 5)) ^ gsw);
   };
-  int offA_h[8], offB_h[2][FBW], offG_h[2];
-  if constexpr (kHoist) {
-    make_offA(lane, offA_h);
-    make_offBG(lane, offB_h, offG_h);
-  }
 
   double ds_acc = 0.0;
   f32x16 dacc[2 * FBW];
@@ -157,12 +150,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
   // DMA of tile dtile's log-sum-exp slot
   auto gemm1 = [&](const INFCL_LDS char* cur, int dtile, INFCL_LDS float* dlse) {
     int offA[8];
-    if constexpr (kHoist) {
-#pragma unroll
-      for (int k = 0; k < 8; ++k) offA[k] = offA_h[k];
-    } else {
-      make_offA(opaque_lane(), offA);
-    }
+    make_offA(opaque_lane(), offA);
     const INFCL_LDS char* half = cur + kSeg * (kh * KH / 8);
     const u32x4 drl = lse_rsrc(dtile);
     f32x16 sacc;
@@ -240,16 +228,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
   // features (transposing reads of the segment-blocked tile)
   auto gemm2 = [&](const INFCL_LDS char* cur) {
     int offB[2][FBW], offG[2];
-    if constexpr (kHoist) {
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int fbw = 0; fbw < FBW; ++fbw) offB[t][fbw] = offB_h[t][fbw];
-      offG[0] = offG_h[0];
-      offG[1] = offG_h[1];
-    } else {
-      make_offBG(opaque_lane(), offB, offG);
-    }
+    make_offBG(opaque_lane(), offB, offG);
     auto readB = [&](int g, s16x4 (&bq)[2]) {
       const int s2 = g / FBW;
 #pragma unroll
@@ -361,17 +340,10 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
 // swept log-sum-exp values a lane needs for tile t are loaded into registers
 // in iteration t-1.
 // At d = 1024 three tiles (3 x 64 KiB) do not fit in LDS: bwd_wide serves it.
-// It is also used at d = 768 only while the swept matrix (b d 2 bytes) is at
-// most kPipeSweptBytes: measured against bwd_wide, it is 2.7% faster at
-// 192 MiB of swept rows (b = 131072) and 4.9-5.2% slower at 240 MiB,
-// 384 MiB and 1.5 GiB (b = 163840, 262144, 1048576), where the tile DMA
-// arrives from beyond the 256 MiB last-level cache: bwd_wide's DMA, paced by
-// the G' work it is interleaved with, tolerates that latency; the burst here
-// does not (an L2 prefetch of the tile ahead made it slower still).
-#ifndef INFCL_PIPE_SWEPT_MIB
-#define INFCL_PIPE_SWEPT_MIB 200
-#endif
-constexpr int64_t kPipeSweptBytes = (int64_t)INFCL_PIPE_SWEPT_MIB << 20;
+// It serves d = 768 at every batch size: measured against bwd_wide, 4% faster
+// at b = 131072 (192 MiB of swept rows, inside the 256 MiB last-level
+// cache) and 1.5-1.6% faster at b = 163840, 262144 and 1048576, where the
+// tiles come from HBM.
 template <int D, bool F16>
 __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
   constexpr int KS = D / 16;
@@ -676,17 +648,10 @@ int bwd_wide_workgroups(int64_t nown) { return (int)((nown + kWideBM - 1) / kWid
 int launch_bwd_wide(const BwdParams& p, int nwg, bool f16, hipStream_t stream) {
   switch (p.d) {
     case 768:
-      if (p.b * 768 * 2 <= kPipeSweptBytes) {
-        if (f16)
-          hipLaunchKernelGGL((bwd_wide3<768, true>), dim3(nwg), dim3(256), 0, stream, p);
-        else
-          hipLaunchKernelGGL((bwd_wide3<768, false>), dim3(nwg), dim3(256), 0, stream, p);
-      } else {
-        if (f16)
-          hipLaunchKernelGGL((bwd_wide<768, true>), dim3(nwg), dim3(256), 0, stream, p);
-        else
-          hipLaunchKernelGGL((bwd_wide<768, false>), dim3(nwg), dim3(256), 0, stream, p);
-      }
+      if (f16)
+        hipLaunchKernelGGL((bwd_wide3<768, true>), dim3(nwg), dim3(256), 0, stream, p);
+      else
+        hipLaunchKernelGGL((bwd_wide3<768, false>), dim3(nwg), dim3(256), 0, stream, p);
       break;
     case 1024:
       if (f16)
