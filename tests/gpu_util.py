@@ -63,4 +63,15 @@ def max_rel(a, ref):
     return float(np.max(np.abs(a - ref)) / m) if m > 0 else float(np.max(np.abs(a)))
 
 
-__all__ = ["device_inputs", "run", "f32_scale", "lse_tol", "max_rel", "synth"]
+def grad_rows(A, B, s, rows, lse_own_rows, lse_other_all, ell_own_rows, ell_other_rows, b):
+    """fp64 rows of dOwn = k G' Other for own rows `rows` (own = A, other = B,
+    k = s / 2b): G'_ij = exp(x_ij - lse_own_i) + exp(x_ij - lse_other_j) off
+    the diagonal, expm1(-ell_own_i) + expm1(-ell_other_i) on it."""
+    k = s / (2.0 * b)
+    x = s * (A[rows] @ B.T)
+    g = np.exp(x - lse_own_rows[:, None]) + np.exp(x - lse_other_all[None, :])
+    g[np.arange(len(rows)), rows] = np.expm1(-ell_own_rows) + np.expm1(-ell_other_rows)
+    return k * (g @ B)
+
+
+__all__ = ["device_inputs", "run", "f32_scale", "grad_rows", "lse_tol", "max_rel", "synth"]

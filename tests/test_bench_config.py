@@ -18,18 +18,9 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_util import f32_scale, lse_tol, max_rel, run, synth
+from gpu_util import f32_scale, grad_rows, lse_tol, max_rel, run, synth
 
 pytestmark = pytest.mark.gpu
-
-
-def _grad_rows(A, B, s, rows, lse_own_rows, lse_other_all, ell_own_rows, ell_other_rows, b):
-    """fp64 rows of dOwn = k * G' Other for own rows `rows` (own = A, other = B)."""
-    k = s / (2.0 * b)
-    x = s * (A[rows] @ B.T)
-    g = np.exp(x - lse_own_rows[:, None]) + np.exp(x - lse_other_all[None, :])
-    g[np.arange(len(rows)), rows] = np.expm1(-ell_own_rows) + np.expm1(-ell_other_rows)
-    return k * (g @ B)
 
 
 @pytest.mark.parametrize("cfg", [4])
@@ -57,8 +48,8 @@ def test_full_size_sampled(cfg):
     # the loss is the mean of the per-sample terms the GPU exported
     assert g["loss64"] == pytest.approx((math.fsum(g["ell_r"]) + math.fsum(g["ell_c"])) / (2 * b), rel=1e-6)
     # gradient rows
-    dI_ref = _grad_rows(I, T, s, rows, sr["lse"], g["lse_c"], sr["ell"], g["ell_c"][rows], b)
-    dT_ref = _grad_rows(T, I, s, rows, sc["lse"], g["lse_r"], sc["ell"], g["ell_r"][rows], b)
+    dI_ref = grad_rows(I, T, s, rows, sr["lse"], g["lse_c"], sr["ell"], g["ell_c"][rows], b)
+    dT_ref = grad_rows(T, I, s, rows, sc["lse"], g["lse_r"], sc["ell"], g["ell_r"][rows], b)
     e1, e2 = max_rel(g["dI"][rows], dI_ref), max_rel(g["dT"][rows], dT_ref)
     print(f"  dI rows {e1:.2e} dT rows {e2:.2e}", flush=True)
     assert e1 <= 2e-2 and e2 <= 2e-2
