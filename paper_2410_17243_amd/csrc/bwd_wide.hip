@@ -435,6 +435,37 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
     return rsrc_words((const char*)p.swept + j0 * ROWG, jt < 0 ? 0 : (b - j0) * ROWG);
   };
   auto tbuf = [&](int t) { return tiles + TILEB * (t % 3); };
+  // The fragment addresses of GEMM1 in the buffer stage 1 reads next (pA)
+  // and of GEMM2 in the buffer stage 2 reads next (pB), advanced with the
+  // buffer rotation before the barrier that ends each iteration, so that no
+  // address arithmetic sits between a barrier and the MFMAs after it.
+  const INFCL_LDS char* pA[8];
+  const INFCL_LDS char* pB[2][FBW];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) pA[k] = tbuf(0) + kSeg * (kh * KH / 8) + offA[k];
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+    for (int fbw = 0; fbw < FBW; ++fbw) pB[tt][fbw] = tbuf(0) + offB[tt][fbw];
+  auto rot = [&](int t) { return TILEB * ((t + 1) % 3 - t % 3); };  // buffer of tile t -> of tile t+1
+  auto advance_pA = [&](int t1) {
+    const int delta = rot(t1);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      pA[k] += delta;
+      asm volatile("" : "+v"(pA[k]));
+    }
+  };
+  auto advance_pB = [&](int t) {
+    const int delta = rot(t);
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int fbw = 0; fbw < FBW; ++fbw) {
+        pB[tt][fbw] += delta;
+        asm volatile("" : "+v"(pB[tt][fbw]));
+      }
+  };
   // DMA instruction kk of tile jt into its buffer
   auto dma_part = [&](int jt, int kk) {
     dma16_asm(tile_rsrc(jt < ntile ? jt : -1), tbuf(jt) + 1024 * (wave + 4 * kk),
@@ -474,20 +505,19 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
   // half); between its MFMAs, the G' entries of tile t from the joined values
   // x (LSE values L0, L1 read from tile t's slot).  Returns the accumulator
   // of tile t1.
-  auto stage1 = [&](int t1, const float (&x)[8], const f32x4& L0, const f32x4& L1, float (&gv)[8], float& ds_t,
+  auto stage1 = [&](const float (&x)[8], const f32x4& L0, const f32x4& L1, float (&gv)[8], float& ds_t,
                     bool with_gp) {
-    const INFCL_LDS char* half = tbuf(t1) + kSeg * (kh * KH / 8);
     f32x16 sacc;
     bf16x8 ring[kPre];
 #pragma unroll
-    for (int i = 0; i < kPre; ++i) ring[i] = *(const INFCL_LDS bf16x8*)(half + offA[i & 7] + kSeg * (i >> 3));
+    for (int i = 0; i < kPre; ++i) ring[i] = *(const INFCL_LDS bf16x8*)(pA[i & 7] + kSeg * (i >> 3));
     __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
 #pragma unroll
     for (int s2 = 0; s2 < KH; ++s2) {
       mfma16_vgpr<F16>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KH - 1);
       if (s2 + kPre < KH) {
         const int n = s2 + kPre;
-        ring[s2 % kPre] = *(const INFCL_LDS bf16x8*)(half + offA[n & 7] + kSeg * (n >> 3));
+        ring[s2 % kPre] = *(const INFCL_LDS bf16x8*)(pA[n & 7] + kSeg * (n >> 3));
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
       if (with_gp && s2 % 3 == 1) {
@@ -504,14 +534,12 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
 
   // ---- stage 2: GEMM2 of tile t (all 64 own rows' G' x this wave's quarter of
   // the tile's features, transposing reads two groups ahead)
-  auto stage2 = [&](int t) {
-    const INFCL_LDS char* cur = tbuf(t);
+  auto stage2 = [&]() {
     auto readB = [&](int g, s16x4 (&bq)[2]) {
       const int s2 = g / FBW;
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
-        bq[tt] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (INFCL_LDS s16x4*)(cur + offB[tt][g % FBW] + 16 * kSegRow * s2));
+        bq[tt] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFCL_LDS s16x4*)(pB[tt][g % FBW] + 16 * kSegRow * s2));
     };
     bf16x8 A[2];
     s16x4 bq[3][2];
@@ -547,7 +575,8 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
     float gv0[8], ds0 = 0.f;
     const f32x4 z = {0.f, 0.f, 0.f, 0.f};
     float x0[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    const f32x16 sacc = stage1(0, x0, z, z, gv0, ds0, false);
+    const f32x16 sacc = stage1(x0, z, z, gv0, ds0, false);
+    advance_pA(0);
     float mine[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) mine[i] = sacc[i];
@@ -570,7 +599,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
     {
       const f32x4 L0 = Lc0, L1 = Lc1;
       float gv[8], ds_t = 0.f;
-      const f32x16 sacc = stage1(t + 1, x, L0, L1, gv, ds_t, true);
+      const f32x16 sacc = stage1(x, L0, L1, gv, ds_t, true);
       const int64_t j0 = (int64_t)t * kBwdBN;
       if ((j0 == own0) || (j0 + kBwdBN > b) || !wave_rows_ok) {
         // tile on the diagonal or past the ragged end: masked entries
@@ -603,13 +632,15 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
     }
     __syncthreads();  // G' block of tile t complete; join data of tile t+1 visible
     // ---- stage 2
-    stage2(t);
+    stage2();
     {
       const f32x4 q0 = *(const INFCL_LDS f32x4*)&xs_[wave ^ 1][lane][0];
       const f32x4 q1 = *(const INFCL_LDS f32x4*)&xs_[wave ^ 1][lane][4];
 #pragma unroll
       for (int i = 0; i < 8; ++i) x[i] = mine[i] + (i < 4 ? q0[i] : q1[i - 4]);
     }
+    advance_pA(t + 1);
+    advance_pB(t);
     wait_dma();
     __syncthreads();  // tile t+2 landed; tile t's buffer, the G' block and the join area are free
     Lc0 = Ln0;
