@@ -129,11 +129,11 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   // k >> 3, rows 4 (k & 7) .. +3; lane L fills row 4 (k & 7) + (L >> 4), physical
   // chunk L & 15, i.e. logical chunk (L & 15) ^ g(row).  Since g(row) =
   // 4 (L >> 4) + (k & 3) and k & 3 = wave, the per-lane part of every source
-  // offset is one constant and the rest is wave-uniform.  Lane offsets are
-  // rebuilt from an opaque lane id at each use: a value held across the loop
-  // can be spilled where registers are short, and a scratch reload waits for
-  // all DMA in flight.  Rows past b fall outside the resource and load as
-  // zeros (their G' is masked); jt < 0 loads zeros only.
+  // offset is one constant and the rest is wave-uniform.  The DMA lane offsets
+  // are rebuilt from an opaque lane id at each use: all 512 registers are in
+  // use at d = 512, a value held across the loop would be spilled, and a
+  // scratch reload waits for all DMA in flight.  Rows past b fall outside the
+  // resource and load as zeros (their G' is masked); jt < 0 loads zeros only.
   auto dma_lane_off = [&]() { return sweep_dma_lane_off(opaque_lane(), wave, ROWG); };
   auto dma_kk_off = [&](int kk) { return sweep_dma_kk_off(kk, wave, ROWG); };
   auto tile_rsrc = [&](int jt) {
@@ -158,7 +158,7 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   };
 
   // ---- per-lane LDS offsets of GEMM1's swept fragments; every read is one
-  // of these plus an immediate (rebuilt per tile from an opaque lane id)
+  // of these plus an immediate
   auto make_offA = [&](int lo, int (&offA)[8]) {
     const int l32o = lo & 31, ho = lo >> 5;
     const int rA = sweep_perm(l32o);
@@ -176,10 +176,21 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   // LDS fragments are read kPre steps ahead of their MFMA through a register
   // ring.  With with_dma, the loads of tile dtile into (ddst, dlse) are issued
   // between the MFMAs, one 1 KiB instruction per KS / NIW steps.
+  // 16-bit inputs: GEMM1's fragment offsets are computed once and held in
+  // registers (rebuilt per tile they cost about 2.5% of the backward at
+  // d = 512; the fp32 form has no registers to spare and rebuilds them)
+  constexpr bool HA = ES == 2;
+  int offA_h[8];
+  if constexpr (HA) make_offA(lane, offA_h);
   auto gemm1 = [&](const INFCL_LDS char* cur, bool with_dma, int dtile, INFCL_LDS char* ddst,
                    INFCL_LDS float* dlse) {
     int offA[8];
-    make_offA(opaque_lane(), offA);
+    if constexpr (HA) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) offA[k] = offA_h[k];
+    } else {
+      make_offA(opaque_lane(), offA);
+    }
     u32x4 drs = tile_rsrc(-1), drl = lse_rsrc(-1);
     uint32_t dlo = 0;
     if (with_dma) {
@@ -289,6 +300,27 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
       *(INFCL_LDS bf16x8*)(gpb + row * 64 + 16 * ((2 * s2 + (lo >> 5)) ^ ((row >> 2) & 3))) = ga[s2];
   };
 
+  // GEMM2's per-lane offsets, computed once where the sweep makes one pass
+  // (its feature blocks are then fixed): another 2.5% at d = 512
+  constexpr bool HB = ES == 2 && NPASS == 1;
+  int offBh[2][FBW], offGh[2];
+  if constexpr (HB) {
+    const int g4 = lane >> 4, l16 = lane & 15;
+    const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
+    const int lb = 2 * nb16 + (qq >> 1);
+    const int fo = (qq & 1) * 8;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int fbw = 0; fbw < FBW; ++fbw) {
+        const int fbabs = wave * FBW + fbw;
+        offBh[t][fbw] = (8 * hh + 4 * t + e) * kSegRow + kSeg * (fbabs >> 2) +
+                        16 * (4 * ((fbabs & 3) ^ e) + (lb ^ ((t + 2 * hh) & 3))) + fo;
+      }
+    const int gsw = (l32 >> 2) & 3;
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) offGh[s2] = l32 * 64 + 16 * ((2 * s2 + h) ^ gsw);
+  }
   for (int pass = 0; pass < NPASS; ++pass) {
     // 16-bit: dacc[ob * FBW + fbw] holds own block ob (rows 32 ob .. of the
     // workgroup) x feature block (pass FB + wave FBW + fbw).
@@ -325,15 +357,16 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
       auto readA = [&](int s2, bf16x8 (&A)[4]) {
 #pragma unroll
         for (int ob = 0; ob < 4; ++ob)
-          A[ob] = *(const INFCL_LDS bf16x8*)(gpb + 2048 * ob + gpo + 16 * ((2 * s2 + ho) ^ gsw));
+          A[ob] = *(const INFCL_LDS bf16x8*)(gpb + 2048 * ob + (HB ? offGh[s2] : gpo + 16 * ((2 * s2 + ho) ^ gsw)));
       };
       auto readB = [&](int g, s16x4 (&bq)[2]) {
         const int s2 = g / FBW, fbw = g % FBW;
         const int fbabs = pass * FB + wave * FBW + fbw;
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-          const int off = (8 * hh + 4 * t + e + 16 * s2) * kSegRow + kSeg * (fbabs >> 2) +
-                          16 * (4 * ((fbabs & 3) ^ e) + (lb ^ ((t + 2 * hh) & 3))) + fo;
+          const int off = HB ? offBh[t][fbw] + 16 * s2 * kSegRow
+                             : (8 * hh + 4 * t + e + 16 * s2) * kSegRow + kSeg * (fbabs >> 2) +
+                                   16 * (4 * ((fbabs & 3) ^ e) + (lb ^ ((t + 2 * hh) & 3))) + fo;
           bq[t] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFCL_LDS s16x4*)(cur + off));
         }
       };
