@@ -471,6 +471,10 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
     dma16_asm(tile_rsrc(jt < ntile ? jt : -1), tbuf(jt) + 1024 * (wave + 4 * kk),
               dma_lo + sweep_dma_kk_off(kk, wave, ROWG));
   };
+  auto dma_part_w1 = [&](int jt, int kk) {
+    dma16_asm_w1(tile_rsrc(jt < ntile ? jt : -1), tbuf(jt) + 1024 * (wave + 4 * kk),
+                 dma_lo + sweep_dma_kk_off(kk, wave, ROWG));
+  };
   // The log-sum-exp values of the 8 swept rows 16 kh + 8 h + i of tile jt
   // whose G' entries the lane forms go straight into registers, one tile
   // ahead (range-checked buffer loads: zeros past b).  Through an LDS slot
@@ -628,7 +632,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
       *(INFCL_LDS f32x4*)&xs_[wave][lane][0] = f32x4{sacc[8], sacc[9], sacc[10], sacc[11]};
       *(INFCL_LDS f32x4*)&xs_[wave][lane][4] = f32x4{sacc[12], sacc[13], sacc[14], sacc[15]};
 #pragma unroll
-      for (int kk = 0; kk < NIW; ++kk) dma_part(t + 2, kk);
+      for (int kk = 0; kk < NIW; ++kk) dma_part_w1(t + 2, kk);
     }
     __syncthreads();  // G' block of tile t complete; join data of tile t+1 visible
     // ---- stage 2

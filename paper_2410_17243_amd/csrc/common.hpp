@@ -140,6 +140,14 @@ __device__ __forceinline__ void dma16_asm(const u32x4& rs, const INFCL_LDS void*
   asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds" ::"v"(voff), "s"(rs), "s"(so), "{m0}"(m0v));
 }
 
+// The same with one wait state only (m0 written by a scalar instruction just
+// before), for bursts whose other operands are set up well ahead; the build's
+// wait-state check verifies every use.
+__device__ __forceinline__ void dma16_asm_w1(const u32x4& rs, const INFCL_LDS void* lds_base, uint32_t voff) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds_base);
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff), "s"(rs), "{m0}"(m0v));
+}
+
 // Merge of two base-2 log-sum-exp pairs (R, l) -> (max R, rescaled sum).
 __device__ __forceinline__ void lse2_merge(float& R, float& l, float R2, float l2) {
   float M = fmaxf(R, R2);
