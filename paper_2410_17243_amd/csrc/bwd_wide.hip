@@ -201,7 +201,13 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
 #pragma unroll
       for (int u = 0; u < (NIW + 7) / 8; ++u) {  // DMA instructions i, i + 8, ...
         const int kk = i + 8 * u;
-        if (kk < NIW) dma16_asm(drs, ddst + 1024 * (wave + 4 * kk), dlo + sweep_dma_kk_off(kk, wave, ROWG));
+        // the lane offset in a VGPR, the instruction's part as the scalar
+        // offset: only the first instruction follows the lane offset's
+        // arithmetic closely enough to need the full padding
+        if (kk == 0)
+          dma16_asm(drs, ddst + 1024 * wave, dlo, sweep_dma_kk_off(0, wave, ROWG));
+        else if (kk < NIW)
+          dma16_asm_w1(drs, ddst + 1024 * (wave + 4 * kk), dlo, sweep_dma_kk_off(kk, wave, ROWG));
       }
       const float x = mine[i] + (i < 4 ? q0[i] : q1[i - 4]);
       const float Lj = i < 4 ? L0[i] : L1[i - 4];

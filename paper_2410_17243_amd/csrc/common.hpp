@@ -147,6 +147,12 @@ __device__ __forceinline__ void dma16_asm_w1(const u32x4& rs, const INFCL_LDS vo
   const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds_base);
   asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff), "s"(rs), "{m0}"(m0v));
 }
+__device__ __forceinline__ void dma16_asm_w1(const u32x4& rs, const INFCL_LDS void* lds_base, uint32_t voff,
+                                             uint32_t soff) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds_base);
+  const uint32_t so = __builtin_amdgcn_readfirstlane(soff);
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds" ::"v"(voff), "s"(rs), "s"(so), "{m0}"(m0v));
+}
 
 // Merge of two base-2 log-sum-exp pairs (R, l) -> (max R, rescaled sum).
 __device__ __forceinline__ void lse2_merge(float& R, float& l, float R2, float l2) {
