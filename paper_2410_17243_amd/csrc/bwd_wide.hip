@@ -29,6 +29,7 @@
 // Three barriers per tile (join, G' block, buffer turn-over).
 #include "bwd.hpp"
 
+
 namespace infcl {
 
 constexpr int kWideBM = 64;  // own rows per workgroup
@@ -160,7 +161,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
     __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
 #pragma unroll
     for (int s2 = 0; s2 < KH; ++s2) {
-      mfma16_vgpr<F16>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KH - 1);
+      mfma16_vgpr<F16, false>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KH - 1);  // unpadded: scan-checked
       if (s2 == 1) dma16_asm(drl, dlse, lse_lane_off());
       if (s2 + kPre < KH) {
         const int n = s2 + kPre;
@@ -524,7 +525,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
     __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
 #pragma unroll
     for (int s2 = 0; s2 < KH; ++s2) {
-      mfma16_vgpr<F16>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KH - 1);
+      mfma16_vgpr<F16, false>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KH - 1);  // unpadded: scan-checked
       if (s2 + kPre < KH) {
         const int n = s2 + kPre;
         ring[s2 % kPre] = *(const INFCL_LDS bf16x8*)(pA[n & 7] + kSeg * (n >> 3));

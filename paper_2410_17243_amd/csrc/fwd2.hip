@@ -45,6 +45,7 @@
 
 #include "sweep.hpp"
 
+
 namespace infcl {
 
 // f(std::integral_constant<int, 0>), ..., f(std::integral_constant<int, N-1>):
@@ -88,21 +89,29 @@ __host__ __device__ constexpr int fwd2_waves(int64_t d) { return d > 512 ? 4 : k
 constexpr float kTinyBound = 5.421010862427522e-20f;  // 2^-64
 // mfma16_vgpr with the B operand (the own rows) held in AGPRs, for d > 512;
 // the same wait states around the MFMA.
-#define INFCL_MFMA16_AB(OP)                                                                                    \
+#define INFCL_MFMA16_AB(PRE, OP)                                                                                \
   if (first && last)                                                                                           \
-    asm volatile("s_nop 1\n\t" OP " %0, %1, %2, 0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3" : "=&v"(acc) : "v"(a), "a"(b)); \
+    asm volatile(PRE OP " %0, %1, %2, 0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3" : "=&v"(acc) : "v"(a), "a"(b));   \
   else if (first)                                                                                              \
-    asm volatile("s_nop 1\n\t" OP " %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "a"(b));                              \
+    asm volatile(PRE OP " %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "a"(b));                                        \
   else if (last)                                                                                               \
-    asm volatile("s_nop 1\n\t" OP " %0, %1, %2, %0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3" : "+v"(acc) : "v"(a), "a"(b)); \
+    asm volatile(PRE OP " %0, %1, %2, %0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3" : "+v"(acc) : "v"(a), "a"(b));  \
   else                                                                                                         \
-    asm volatile("s_nop 1\n\t" OP " %0, %1, %2, %0" : "+v"(acc) : "v"(a), "a"(b));
-template <bool F16>
+    asm volatile(PRE OP " %0, %1, %2, %0" : "+v"(acc) : "v"(a), "a"(b));
+template <bool F16, bool PAD = true>
 __device__ __forceinline__ void mfma16_vgpr_ab(f32x16& acc, const bf16x8& a, const bf16x8& b, bool first, bool last) {
   if constexpr (F16) {
-    INFCL_MFMA16_AB("v_mfma_f32_32x32x16_f16")
+    if constexpr (PAD) {
+      INFCL_MFMA16_AB("s_nop 1\n\t", "v_mfma_f32_32x32x16_f16")
+    } else {
+      INFCL_MFMA16_AB("", "v_mfma_f32_32x32x16_f16")
+    }
   } else {
-    INFCL_MFMA16_AB("v_mfma_f32_32x32x16_bf16")
+    if constexpr (PAD) {
+      INFCL_MFMA16_AB("s_nop 1\n\t", "v_mfma_f32_32x32x16_bf16")
+    } else {
+      INFCL_MFMA16_AB("", "v_mfma_f32_32x32x16_bf16")
+    }
   }
 }
 #undef INFCL_MFMA16_AB
@@ -370,12 +379,14 @@ __global__ void __launch_bounds__(64 * fwd2_waves(D), D > 512 ? 1 : 2) fwd_sweep
 #pragma unroll
       for (int i = 0; i < kPre; ++i) ring[i] = *(const INFCL_LDS bf16x8*)(cur + offA[i & 7] + kSeg * (i >> 3));
       __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
+      // (MFMAs without leading padding: their sources are LDS loads and the
+      // own rows loaded before the sweep, which the build's scan confirms)
       static_for<KS>([&](auto s2c) {
         constexpr int s2 = decltype(s2c)::value;
         if constexpr (D > 512)  // own rows in AGPRs
-          mfma16_vgpr_ab<F16>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KS - 1);
+          mfma16_vgpr_ab<F16, false>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KS - 1);
         else
-          mfma16_vgpr<F16>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KS - 1);
+          mfma16_vgpr<F16, false>(sacc, ring[s2 % kPre], ownf[s2], s2 == 0, s2 == KS - 1);
         constexpr int SPI = KS / NIW;  // steps per DMA instruction
         if ((s2 + 1) % SPI == 0) {
           const int kk = kk0 + (s2 + 1) / SPI - 1;

@@ -50,22 +50,34 @@ __device__ __forceinline__ uint32_t sweep_dma_kk_off(int kk, int wave, int rowg)
 // v_accvgpr_read, must be two wait states old), and the last MFMA of a chain
 // is followed by the wait states a VALU read of its result needs, inside the
 // same statement so that nothing reads the accumulator earlier.
-#define INFCL_MFMA16_VGPR(OP)                                                                                  \
+#define INFCL_MFMA16_VGPR(PRE, OP)                                                                              \
   if (first && last)                                                                                           \
-    asm volatile("s_nop 1\n\t" OP " %0, %1, %2, 0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3" : "=&v"(acc) : "v"(a), "v"(b)); \
+    asm volatile(PRE OP " %0, %1, %2, 0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3" : "=&v"(acc) : "v"(a), "v"(b));   \
   else if (first)                                                                                              \
-    asm volatile("s_nop 1\n\t" OP " %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "v"(b));                              \
+    asm volatile(PRE OP " %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "v"(b));                                        \
   else if (last)                                                                                               \
-    asm volatile("s_nop 1\n\t" OP " %0, %1, %2, %0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3" : "+v"(acc) : "v"(a), "v"(b)); \
+    asm volatile(PRE OP " %0, %1, %2, %0\n\ts_nop 7\n\ts_nop 7\n\ts_nop 3" : "+v"(acc) : "v"(a), "v"(b));  \
   else                                                                                                         \
-    asm volatile("s_nop 1\n\t" OP " %0, %1, %2, %0" : "+v"(acc) : "v"(a), "v"(b));
+    asm volatile(PRE OP " %0, %1, %2, %0" : "+v"(acc) : "v"(a), "v"(b));
 
-template <bool F16>
+// PAD = false drops the two leading wait states, for call sites whose source
+// operands are never written by a VALU instruction just before (LDS loads and
+// registers set up before the sweep); the build's wait-state scan checks
+// every site of either form.
+template <bool F16, bool PAD = true>
 __device__ __forceinline__ void mfma16_vgpr(f32x16& acc, const bf16x8& a, const bf16x8& b, bool first, bool last) {
   if constexpr (F16) {
-    INFCL_MFMA16_VGPR("v_mfma_f32_32x32x16_f16")
+    if constexpr (PAD) {
+      INFCL_MFMA16_VGPR("s_nop 1\n\t", "v_mfma_f32_32x32x16_f16")
+    } else {
+      INFCL_MFMA16_VGPR("", "v_mfma_f32_32x32x16_f16")
+    }
   } else {
-    INFCL_MFMA16_VGPR("v_mfma_f32_32x32x16_bf16")
+    if constexpr (PAD) {
+      INFCL_MFMA16_VGPR("s_nop 1\n\t", "v_mfma_f32_32x32x16_bf16")
+    } else {
+      INFCL_MFMA16_VGPR("", "v_mfma_f32_32x32x16_bf16")
+    }
   }
 }
 #undef INFCL_MFMA16_VGPR
