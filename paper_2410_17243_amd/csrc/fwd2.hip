@@ -250,6 +250,12 @@ __global__ void __launch_bounds__(64 * fwd2_waves(D), D > 512 ? 1 : 2) fwd_sweep
   // lane, the column-pair slot offset, and GEMM1's swept fragment offsets
   // (tile base + kSeg (n >> 3) + offA[n & 7]).
   const uint32_t dma_lo = sweep_dma_lane_off(lane, wq, ROWG);
+  // d > 512 (registers to spare): the full source offset of each of the
+  // wave's DMA instructions, computed once, so that no VALU instruction
+  // writes a DMA operand inside the sweep and the DMA needs one wait state
+  uint32_t dvo[D > 512 ? NIW : 1];
+#pragma unroll
+  for (int k = 0; k < (D > 512 ? NIW : 1); ++k) dvo[k] = dma_lo + sweep_dma_kk_off(kk0 + k, wq, ROWG);
   const uint32_t slot_lo = 16u * (uint32_t)(lane & 7);
   int offA[8];
   {
@@ -390,7 +396,10 @@ __global__ void __launch_bounds__(64 * fwd2_waves(D), D > 512 ? 1 : 2) fwd_sweep
         constexpr int SPI = KS / NIW;  // steps per DMA instruction
         if ((s2 + 1) % SPI == 0) {
           const int kk = kk0 + (s2 + 1) / SPI - 1;
-          dma16_asm(drs, nxt + 1024 * (wq + 4 * kk), dma_lo + sweep_dma_kk_off(kk, wq, ROWG));
+          if constexpr (D > 512)
+            dma16_asm_w1(drs, nxt + 1024 * (wq + 4 * kk), dvo[(s2 + 1) / SPI - 1]);
+          else
+            dma16_asm(drs, nxt + 1024 * (wq + 4 * kk), dma_lo + sweep_dma_kk_off(kk, wq, ROWG));
         }
         if (slot_wave && s2 == (KS > 1 ? 1 : 0)) issue_slot(jn, first_rb, snxt);
         if constexpr (s2 + kPre < KS) {
