@@ -216,7 +216,9 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
       __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
 #pragma unroll
       for (int s2 = 0; s2 < KS; ++s2) {
-        mfma16_vgpr<F16>(sacc, ring[s2 % kPre], ownf[s2][0], s2 == 0, s2 == KS - 1);
+        // one pass: no leading padding (its sources are LDS loads and the own
+        // rows, never restored just before; the build's scan checks it)
+        mfma16_vgpr<F16, (NPASS > 1)>(sacc, ring[s2 % kPre], ownf[s2][0], s2 == 0, s2 == KS - 1);
         dma_step(s2);
         if (s2 + kPre < KS) {
           const int n = s2 + kPre;
