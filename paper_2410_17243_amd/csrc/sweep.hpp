@@ -45,8 +45,8 @@ __device__ __forceinline__ uint32_t sweep_dma_kk_off(int kk, int wave, int rowg)
 // compiler would place an accumulation chain in AGPRs, which the backward
 // needs for its gradients).  Volatile, so that the chain keeps its order with
 // interleaved DMA instructions.  Hazards inside inline assembly are not
-// checked by the compiler: two wait states precede each MFMA (a VALU write of
-// a source operand, e.g. an operand the compiler restores with
+// checked by the compiler: with PAD, two wait states precede each MFMA (a
+// VALU write of a source operand, e.g. an operand the compiler restores with
 // v_accvgpr_read, must be two wait states old), and the last MFMA of a chain
 // is followed by the wait states a VALU read of its result needs, inside the
 // same statement so that nothing reads the accumulator earlier.
