@@ -205,7 +205,7 @@ __global__ void __launch_bounds__(64 * fwd2_waves(D), D > 512 ? 1 : 2) fwd_sweep
 #define INFCL_F2_PRE 4
 #endif
 #ifndef INFCL_F2_PRE_WIDE
-#define INFCL_F2_PRE_WIDE 8
+#define INFCL_F2_PRE_WIDE 6
 #endif
   constexpr int kPreD = D > 512 ? INFCL_F2_PRE_WIDE : INFCL_F2_PRE;
   constexpr int kPre = KS < kPreD ? KS : kPreD;
