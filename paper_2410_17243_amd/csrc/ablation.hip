@@ -162,9 +162,8 @@ __global__ void __launch_bounds__(256, 1) bwd_single(SingleParams p) {
     {
       const int lo = opaque_lane();
       const int rA = sweep_perm(lo & 31);
-      const int gA = sweep_g(rA);
 #pragma unroll
-      for (int k = 0; k < 8; ++k) offA[k] = rA * kSegRow + 16 * ((2 * k + (lo >> 5)) ^ gA);
+      for (int k = 0; k < 8; ++k) offA[k] = sweep_seg_off(rA, 2 * k + (lo >> 5));
     }
     const INFCL_LDS char* half = cur + kSeg * (kh * KH / 8);
     f32x16 sacc;
@@ -237,34 +236,27 @@ __global__ void __launch_bounds__(256, 1) bwd_single(SingleParams p) {
       ga[i] = (__bf16)gg;
     }
     const int row = 32 * ob + l32;
-    *(INFCL_LDS bf16x8*)(gp + row * 64 + 16 * ((2 * kh + h) ^ ((row >> 2) & 3))) = ga;
+    *(INFCL_LDS bf16x8*)(gp + gp_chunk_off(row, 2 * kh + h)) = ga;
     return ds_tile;
   };
 
   // ---- dI: all 64 own rows' G' x this wave's quarter of the tile's features
   auto gemm2 = [&](const INFCL_LDS char* cur) {
     const int lo = opaque_lane();
-    const int l32o = lo & 31, ho = lo >> 5;
-    const int g4 = lo >> 4, l16 = lo & 15;
-    const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
-    const int lb = 2 * nb16 + (qq >> 1);
-    const int fo = (qq & 1) * 8;
-    const int gpo = l32o * 64;
-    const int gsw = (l32o >> 2) & 3;
+    const int ho = lo >> 5;
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
       bf16x8 A[2];
 #pragma unroll
       for (int o2 = 0; o2 < 2; ++o2)
-        A[o2] = *(const INFCL_LDS bf16x8*)(gp + 2048 * o2 + gpo + 16 * ((2 * s2 + ho) ^ gsw));
+        A[o2] = *(const INFCL_LDS bf16x8*)(gp + 2048 * o2 + gp_chunk_off(lo & 31, 2 * s2 + ho));
 #pragma unroll
       for (int fbw = 0; fbw < FBW; ++fbw) {
         const int fbabs = wave * FBW + fbw;
         s16x4 bq[2];
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-          const int off = (8 * hh + 4 * t + e + 16 * s2) * kSegRow + kSeg * (fbabs >> 2) +
-                          16 * (4 * ((fbabs & 3) ^ e) + (lb ^ ((t + 2 * hh) & 3))) + fo;
+          const int off = sweep_tr_off(lo, t, fbabs) + 16 * kSegRow * s2;
           bq[t] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFCL_LDS s16x4*)(cur + off));
         }
         const s16x8 bb = {bq[0][0], bq[0][1], bq[0][2], bq[0][3], bq[1][0], bq[1][1], bq[1][2], bq[1][3]};

@@ -162,12 +162,8 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   auto make_offA = [&](int lo, int (&offA)[8]) {
     const int l32o = lo & 31, ho = lo >> 5;
     const int rA = sweep_perm(l32o);
-    const int gA = sweep_g(rA);
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int cl = ES == 2 ? (2 * k + ho) : (4 * (k >> 1) + 2 * ho + (k & 1));
-      offA[k] = rA * kSegRow + 16 * (cl ^ gA);
-    }
+    for (int k = 0; k < 8; ++k) offA[k] = sweep_seg_off(rA, ES == 2 ? (2 * k + ho) : (4 * (k >> 1) + 2 * ho + (k & 1)));
   };
 
   double ds_acc = 0.0;
@@ -299,7 +295,7 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
     const int row = 32 * wave + (lo & 31);
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2)
-      *(INFCL_LDS bf16x8*)(gpb + row * 64 + 16 * ((2 * s2 + (lo >> 5)) ^ ((row >> 2) & 3))) = ga[s2];
+      *(INFCL_LDS bf16x8*)(gpb + gp_chunk_off(row, 2 * s2 + (lo >> 5))) = ga[s2];
   };
 
   // GEMM2's per-lane offsets, computed once where the sweep makes one pass
@@ -307,21 +303,12 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   constexpr bool HB = ES == 2 && NPASS == 1;
   int offBh[2][FBW], offGh[2];
   if constexpr (HB) {
-    const int g4 = lane >> 4, l16 = lane & 15;
-    const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
-    const int lb = 2 * nb16 + (qq >> 1);
-    const int fo = (qq & 1) * 8;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int fbw = 0; fbw < FBW; ++fbw) {
-        const int fbabs = wave * FBW + fbw;
-        offBh[t][fbw] = (8 * hh + 4 * t + e) * kSegRow + kSeg * (fbabs >> 2) +
-                        16 * (4 * ((fbabs & 3) ^ e) + (lb ^ ((t + 2 * hh) & 3))) + fo;
-      }
-    const int gsw = (l32 >> 2) & 3;
+      for (int fbw = 0; fbw < FBW; ++fbw) offBh[t][fbw] = sweep_tr_off(lane, t, wave * FBW + fbw);
 #pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) offGh[s2] = l32 * 64 + 16 * ((2 * s2 + h) ^ gsw);
+    for (int s2 = 0; s2 < 2; ++s2) offGh[s2] = gp_chunk_off(l32, 2 * s2 + h);
   }
   for (int pass = 0; pass < NPASS; ++pass) {
     // 16-bit: dacc[ob * FBW + fbw] holds own block ob (rows 32 ob .. of the
@@ -346,20 +333,14 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
       constexpr int EPS = (16 + NG - 1) / NG;  // G' entries per stage
       constexpr int NL = EPS > 2 ? 4 : 2;      // live log-sum-exp blocks
       const int lo = opaque_lane();
-      const int l32o = lo & 31, ho = lo >> 5;
-      const int g4 = lo >> 4, l16 = lo & 15;
-      const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
-      const int lb = 2 * nb16 + (qq >> 1);
-      const int fo = (qq & 1) * 8;
-      const int gpo = l32o * 64;  // G' row of own block 0; own block ob adds 2048 ob
-      const int gsw = (l32o >> 2) & 3;
+      const int ho = lo >> 5;
       const INFCL_LDS char* lp = (const INFCL_LDS char*)lnext + 32 * ho;
       auto readL = [&](int q4) { return *(const INFCL_LDS f32x4*)(lp + 64 * (q4 >> 1) + 16 * (q4 & 1)); };
       auto first_stage = [](int q) { return (4 * q) / EPS; };  // first stage using LSE block q
       auto readA = [&](int s2, bf16x8 (&A)[4]) {
 #pragma unroll
         for (int ob = 0; ob < 4; ++ob)
-          A[ob] = *(const INFCL_LDS bf16x8*)(gpb + 2048 * ob + (HB ? offGh[s2] : gpo + 16 * ((2 * s2 + ho) ^ gsw)));
+          A[ob] = *(const INFCL_LDS bf16x8*)(gpb + 2048 * ob + (HB ? offGh[s2] : gp_chunk_off(lo & 31, 2 * s2 + ho)));
       };
       auto readB = [&](int g, s16x4 (&bq)[2]) {
         const int s2 = g / FBW, fbw = g % FBW;
@@ -367,8 +348,7 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
           const int off = HB ? offBh[t][fbw] + 16 * s2 * kSegRow
-                             : (8 * hh + 4 * t + e + 16 * s2) * kSegRow + kSeg * (fbabs >> 2) +
-                                   16 * (4 * ((fbabs & 3) ^ e) + (lb ^ ((t + 2 * hh) & 3))) + fo;
+                             : sweep_tr_off(lo, t, fbabs) + 16 * kSegRow * s2;
           bq[t] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFCL_LDS s16x4*)(cur + off));
         }
       };
@@ -428,8 +408,7 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
         for (int r = 0; r < 16; ++r) {
           const int j = sweep_perm(8 * (r >> 2) + 4 * h + (r & 3));
           const int cf = 8 * fbabs + (l32 >> 2);
-          float bv = *(const INFCL_LDS float*)(cur + kSeg * (cf >> 4) + j * kSegRow + 16 * ((cf & 15) ^ sweep_g(j)) +
-                                               (l32 & 3) * 4);
+          float bv = *(const INFCL_LDS float*)(cur + sweep_chunk_off(j, cf) + (l32 & 3) * 4);
           dacc[fb] = mfma_f32(gv[r], bv, dacc[fb]);
         }
       }

@@ -116,28 +116,18 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
   // finishes (tile rows 16 kh + 8 h + i), entries 8..15 the ones it hands over.
   auto make_offA = [&](int lo, int (&o)[8]) {
     const int rA = sweep_perm(lo & 31) ^ (16 * kh);
-    const int gA = sweep_g(rA);
 #pragma unroll
-    for (int k = 0; k < 8; ++k) o[k] = rA * kSegRow + 16 * ((2 * k + (lo >> 5)) ^ gA);
+    for (int k = 0; k < 8; ++k) o[k] = sweep_seg_off(rA, 2 * k + (lo >> 5));
   };
   // GEMM2's transposing reads (tile base + offB[t][fbw] + 16 kSegRow s2) and
   // G' fragments (G' block + offG[s2])
   auto make_offBG = [&](int lo, int (&oB)[2][FBW], int (&oG)[2]) {
-    const int g4 = lo >> 4, l16 = lo & 15;
-    const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
-    const int lb = 2 * nb16 + (qq >> 1);
-    const int fo = (qq & 1) * 8;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int fbw = 0; fbw < FBW; ++fbw) {
-        const int fbabs = wave * FBW + fbw;
-        oB[t][fbw] = (8 * hh + 4 * t + e) * kSegRow + kSeg * (fbabs >> 2) +
-                     16 * (4 * ((fbabs & 3) ^ e) + (lb ^ ((t + 2 * hh) & 3))) + fo;
-      }
-    const int l32o = lo & 31, gsw = (l32o >> 2) & 3;
+      for (int fbw = 0; fbw < FBW; ++fbw) oB[t][fbw] = sweep_tr_off(lo, t, wave * FBW + fbw);
 #pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) oG[s2] = l32o * 64 + 16 * ((2 * s2 + (lo >> 5)) ^ gsw);
+    for (int s2 = 0; s2 < 2; ++s2) oG[s2] = gp_chunk_off(lo & 31, 2 * s2 + (lo >> 5));
   };
 
   double ds_acc = 0.0;
@@ -227,7 +217,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
       ga[i] = to16<F16>(F16 ? gg * g16a : gg);
     }
     const int row = 32 * ob + l32;
-    *(INFCL_LDS bf16x8*)(gp + row * 64 + 16 * ((2 * kh + h) ^ ((row >> 2) & 3))) = ga;
+    *(INFCL_LDS bf16x8*)(gp + gp_chunk_off(row, 2 * kh + h)) = ga;
     return ds_tile;
   };
 
@@ -414,28 +404,18 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
   int offA[8];
   {
     const int rA = sweep_perm(l32) ^ (16 * kh);
-    const int gA = sweep_g(rA);
 #pragma unroll
-    for (int k = 0; k < 8; ++k) offA[k] = rA * kSegRow + 16 * ((2 * k + h) ^ gA);
+    for (int k = 0; k < 8; ++k) offA[k] = sweep_seg_off(rA, 2 * k + h);
   }
   int offB[2][FBW];  // GEMM2's transposing reads: tile base + offB + 16 kSegRow s2
   int offG[2];       // GEMM2's G' fragments of feature step s2
   {
-    const int g4 = lane >> 4, l16 = lane & 15;
-    const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
-    const int lb = 2 * nb16 + (qq >> 1);
-    const int fo = (qq & 1) * 8;
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-      for (int fbw = 0; fbw < FBW; ++fbw) {
-        const int fbabs = wave * FBW + fbw;
-        offB[tt][fbw] = (8 * hh + 4 * tt + e) * kSegRow + kSeg * (fbabs >> 2) +
-                        16 * (4 * ((fbabs & 3) ^ e) + (lb ^ ((tt + 2 * hh) & 3))) + fo;
-      }
-    const int gsw = (l32 >> 2) & 3;
+      for (int fbw = 0; fbw < FBW; ++fbw) offB[tt][fbw] = sweep_tr_off(lane, tt, wave * FBW + fbw);
 #pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) offG[s2] = l32 * 64 + 16 * ((2 * s2 + h) ^ gsw);
+    for (int s2 = 0; s2 < 2; ++s2) offG[s2] = gp_chunk_off(l32, 2 * s2 + h);
   }
   auto tile_rsrc = [&](int jt) {
     const int64_t j0 = (int64_t)(jt < 0 ? 0 : jt) * kBwdBN;
@@ -633,7 +613,7 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) ga[i] = to16<F16>(gv[i]);
       const int row = 32 * ob + l32;
-      *(INFCL_LDS bf16x8*)(gp + row * 64 + 16 * ((2 * kh + h) ^ ((row >> 2) & 3))) = ga;
+      *(INFCL_LDS bf16x8*)(gp + gp_chunk_off(row, 2 * kh + h)) = ga;
 #pragma unroll
       for (int i = 0; i < 8; ++i) mine[i] = sacc[i];
       *(INFCL_LDS f32x4*)&xs_[wave][lane][0] = f32x4{sacc[8], sacc[9], sacc[10], sacc[11]};

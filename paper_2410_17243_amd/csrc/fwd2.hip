@@ -260,9 +260,8 @@ __global__ void __launch_bounds__(64 * fwd2_waves(D), D > 512 ? 1 : 2) fwd_sweep
   int offA[8];
   {
     const int rA = sweep_perm(l32);
-    const int gA = sweep_g(rA);
 #pragma unroll
-    for (int k = 0; k < 8; ++k) offA[k] = rA * kSegRow + 16 * ((2 * k + h) ^ gA);
+    for (int k = 0; k < 8; ++k) offA[k] = sweep_seg_off(rA, 2 * k + h);
   }
   // swept row (tile-relative) of accumulator entry r of this lane
   auto jrow = [&](int r) { return 16 * (r >> 3) + 8 * h + (r & 7); };

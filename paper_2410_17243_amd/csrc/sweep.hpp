@@ -21,11 +21,13 @@ constexpr int kSeg = kSweepBN * kSegRow;
 
 // Chunk swizzle: 16 rows reading one logical chunk, and the 4 rows x 4 chunks
 // of a transposing read, are both spread over all 64 banks.
-__device__ __forceinline__ int sweep_g(int r) { return 4 * (r & 3) + ((r >> 2) & 3); }
+// The index helpers below are host-callable too: a CPU test enumerates every
+// lane, wave and step with them and checks the layout's bounds and coverage.
+__host__ __device__ __forceinline__ int sweep_g(int r) { return 4 * (r & 3) + ((r >> 2) & 3); }
 // Row permutation of the first product: MFMA row m loads swept row perm(m)
 // (bits 2 and 3 swapped), so that accumulator register 8s+t of lane half h
 // holds swept row 16s + 8h + t of the tile.
-__device__ __forceinline__ int sweep_perm(int m) { return (m & 0x13) | ((m & 4) << 1) | ((m & 8) >> 1); }
+__host__ __device__ __forceinline__ int sweep_perm(int m) { return (m & 0x13) | ((m & 4) << 1) | ((m & 8) >> 1); }
 
 // DMA of a swept tile: instruction k = wave + 4 kk fills LDS bytes
 // [1024 k, 1024 k + 1024): segment k >> 3, rows 4 (k & 7) .. +3; lane L fills
@@ -33,13 +35,41 @@ __device__ __forceinline__ int sweep_perm(int m) { return (m & 0x13) | ((m & 4) 
 // (L & 15) ^ sweep_g(row).  Since sweep_g(row) = 4 (L >> 4) + (k & 3) and
 // k & 3 = wave, the per-lane part of every source offset is one constant
 // (lane_off) and the rest is wave-uniform (kk_off).  rowg = bytes per row.
-__device__ __forceinline__ uint32_t sweep_dma_lane_off(int lo, int wave, int rowg) {
+__host__ __device__ __forceinline__ uint32_t sweep_dma_lane_off(int lo, int wave, int rowg) {
   return (uint32_t)((lo >> 4) * rowg + 16 * ((lo & 15) ^ (4 * (lo >> 4)) ^ wave));
 }
-__device__ __forceinline__ uint32_t sweep_dma_kk_off(int kk, int wave, int rowg) {
+__host__ __device__ __forceinline__ uint32_t sweep_dma_kk_off(int kk, int wave, int rowg) {
   const int k = wave + 4 * kk;
   return (uint32_t)(4 * (k & 7) * rowg + 256 * (k >> 3));
 }
+
+// Chunk c (0..15) of row r within its segment: the part of the layout's
+// address below the segment base.
+__host__ __device__ __forceinline__ int sweep_seg_off(int r, int c) { return r * kSegRow + 16 * (c ^ sweep_g(r)); }
+// Chunk c of row r within the tile (any c).
+__host__ __device__ __forceinline__ int sweep_chunk_off(int r, int c) {
+  return kSeg * (c >> 4) + sweep_seg_off(r, c & 15);
+}
+
+// Transposing read of the backward's second product (ds_read_b64_tr_b16):
+// offset of the 8 bytes that lane `lane` reads for row group tt (0 or 1) of
+// 32-feature block fb, contraction rows 0..15 (add 16 kSegRow for rows
+// 16..31).  Lane L reads features 4 (L & 3) .. +3 of the block's 16-feature
+// half (L >> 4) & 1 in row 8 (L >> 5) + 4 tt + ((L & 15) >> 2): 4 rows x 4
+// features per 16-lane group.  The chunk order inside a row group spreads
+// each half-wave's 32 reads over all 64 banks.
+__host__ __device__ __forceinline__ int sweep_tr_off(int lane, int tt, int fb) {
+  const int g4 = lane >> 4, l16 = lane & 15;
+  const int e = l16 >> 2, qq = l16 & 3, nb16 = g4 & 1, hh = g4 >> 1;
+  const int lb = 2 * nb16 + (qq >> 1);
+  const int fo = (qq & 1) * 8;
+  return (8 * hh + 4 * tt + e) * kSegRow + kSeg * (fb >> 2) + 16 * (4 * ((fb & 3) ^ e) + (lb ^ ((tt + 2 * hh) & 3))) +
+         fo;
+}
+
+// G' block of the backward: 64 bytes per own row (32 swept columns, 16-bit),
+// its four 16-byte chunks XOR-swizzled by (row >> 2) & 3.
+__host__ __device__ __forceinline__ int gp_chunk_off(int row, int c) { return row * 64 + 16 * (c ^ ((row >> 2) & 3)); }
 
 // 16-bit 32x32x16 MFMA (bf16, or fp16 with F16) accumulating in VGPRs (the
 // compiler would place an accumulation chain in AGPRs, which the backward
