@@ -32,9 +32,14 @@
  *     enqueued; an invalid call returns a status and launches nothing.  A
  *     launch failure is reported as INFCL_ERR_HIP.  Non-finite input values
  *     are outside the contract (they propagate).
- *   - Supported shapes: 1 <= b <= 2^30; d a multiple of 128 with d <= 1024
- *     for bf16 and f16, a multiple of 64 with d <= 512 for f32
- *     (INFCL_ERR_UNSUPPORTED otherwise).
+ *   - Supported shapes: 1 <= b <= 2^30; d a multiple of 8 with d <= 1024
+ *     for bf16 and f16, a multiple of 4 with d <= 512 for f32 (rows of
+ *     whole 16-byte units; INFCL_ERR_UNSUPPORTED otherwise).  The kernels
+ *     are built for multiples of 128 (16-bit) and 64 (f32); at any other
+ *     width the calls copy img and txt into the workspace with zero features
+ *     appended up to the next such multiple and write the gradients through
+ *     padded buffers there.  Zero features change no dot product: every
+ *     output is exactly that of the unpadded inputs.
  *   - Results are bitwise reproducible for a given (b, d, dtype): no atomics,
  *     all reductions run in a fixed order.
  *   - The calls may be captured into a HIP graph: they enqueue kernels only
@@ -64,8 +69,11 @@ typedef enum {
 typedef enum { INFCL_BF16 = 0, INFCL_F32 = 1, INFCL_F16 = 2 } infcl_dtype;
 
 /* Bytes of device workspace that infcl_fwd / infcl_bwd need for (b, d, dtype).
- * The same workspace size serves both calls.  Returns INFCL_ERR_INVALID for a
- * NULL `bytes` or b < 1, d < 1 or an unknown dtype. */
+ * The same workspace size serves both calls.  It is linear in b: a few
+ * vectors of b floats, plus, when d is not a multiple of 128 (16-bit) or 64
+ * (f32), the padded copies of img and txt and the padded fp32 gradients
+ * (2 b d' elements each, d' the padded width).  Returns INFCL_ERR_INVALID for
+ * a NULL `bytes` or b < 1, d < 1 or an unknown dtype. */
 infcl_status infcl_workspace_size(int64_t b, int64_t d, int dtype, size_t* bytes);
 
 /* Forward pass (Eq. 1-2 with the tiling of Eq. 3-5 / the in-GPU forward

@@ -33,8 +33,23 @@ namespace {
 
 constexpr int64_t kMaxB = (int64_t)1 << 30;
 
+// Widths: the interface takes 16-bit rows of any multiple of 8 features up to
+// 1024 and fp32 rows of any multiple of 4 up to 512 (16-byte rows); the sweeps
+// are built for multiples of 128 (16-bit) and 64 (fp32), and other widths run
+// on zero-padded copies of the inputs in the workspace, the gradients going
+// through padded buffers there too.  Zero features add nothing to any dot
+// product, so every output is that of the unpadded problem; the padding's
+// gradients are zero and are dropped.
+int64_t kernel_width(int64_t d, int dtype) {
+  const int64_t q = dtype == INFCL_F32 ? 64 : 128;
+  return (d + q - 1) / q * q;
+}
+bool width_ok(int64_t d, int dtype) { return dtype == INFCL_F32 ? d % 4 == 0 && d <= 512 : d % 8 == 0 && d <= 1024; }
+size_t elem_size(int dtype) { return dtype == INFCL_F32 ? 4 : 2; }
+
 struct Layout {
-  size_t rowR, rowL, colR, colL, udiag, ref2, fwd_part, lse2, bwd_part, g16, total;
+  int64_t dk;  // the width the sweeps run at
+  size_t rowR, rowL, colR, colL, udiag, ref2, fwd_part, lse2, bwd_part, g16, pad, gpad, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -48,11 +63,12 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // its row partials are nrows long.
 Layout make_layout(int64_t b, int64_t d, int dtype) {
   Layout L;
+  L.dk = kernel_width(d, dtype);
   int Pr = 0, Pc = 0;
   size_t nrow = 0, ncol = 0;
-  const bool resident = infcl::fwd2_supported(d, dtype);
+  const bool resident = infcl::fwd2_supported(L.dk, dtype);
   if (resident) {
-    infcl::fwd2_grid(b, b, d, &Pr, &Pc);
+    infcl::fwd2_grid(b, b, L.dk, &Pr, &Pc);
     nrow = (size_t)Pc;
   } else {
     infcl::fwd1_grid(b, b, &Pr, &Pc);
@@ -71,9 +87,64 @@ Layout make_layout(int64_t b, int64_t d, int dtype) {
   L.lse2 = off; off = align256(off + 2 * fb);
   L.bwd_part = off; off = align256(off + (size_t)2 * ((b + 63) / 64) * sizeof(double));  // 64 or 128 rows per WG
   L.g16 = off; off = align256(off + (dtype == INFCL_F16 ? (size_t)(2 + 2 * ((b + 255) / 256)) * sizeof(float) : 0));
+  L.pad = off; off = align256(off + (L.dk != d ? 2 * (size_t)b * (size_t)L.dk * elem_size(dtype) : 0));  // img, txt
+  L.gpad = off; off = align256(off + (L.dk != d ? 2 * (size_t)b * (size_t)L.dk * sizeof(float) : 0));  // dimg, dtxt
   L.total = off;
   return L;
 }
+
+// Row copy between widths: rows of cin 16-byte chunks into rows of cout
+// chunks, cut or zero-filled at the end.
+__global__ void __launch_bounds__(256) copy_rows(const uint4* __restrict__ src, uint4* __restrict__ dst, int64_t rows,
+                                                 int cin, int cout) {
+  const int64_t n = rows * cout;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = i / cout;
+    const int c = (int)(i - r * cout);
+    dst[i] = c < cin ? src[r * cin + c] : make_uint4(0u, 0u, 0u, 0u);
+  }
+}
+
+unsigned copy_grid(int64_t n) { return (unsigned)(n / 256 + 1 < 65536 ? n / 256 + 1 : 65536); }
+
+// The inputs the sweeps read: img and txt as given, or, when d is not a width
+// the sweeps are built for, their zero-padded copies in the workspace.
+// Returns false on a launch failure.
+bool stage_inputs(const void*& img, const void*& txt, int64_t b, int64_t d, int dtype, char* ws, const Layout& L,
+                  hipStream_t stream) {
+  if (L.dk == d) return true;
+  const int cin = (int)(d * elem_size(dtype) / 16), cout = (int)(L.dk * elem_size(dtype) / 16);
+  const int64_t n = b * cout;
+  uint4* pi = (uint4*)(ws + L.pad);
+  uint4* pt = pi + n;
+  hipLaunchKernelGGL(copy_rows, dim3(copy_grid(n)), dim3(256), 0, stream, (const uint4*)img, pi, b, cin, cout);
+  hipLaunchKernelGGL(copy_rows, dim3(copy_grid(n)), dim3(256), 0, stream, (const uint4*)txt, pt, b, cin, cout);
+  if (hipGetLastError() != hipSuccess) return false;
+  img = pi;
+  txt = pt;
+  return true;
+}
+
+// Where the sweeps write the gradients of `rows` own samples: the caller's
+// dimg and dtxt, or padded buffers in the workspace that unstage_grads then
+// copies, without the padding, into the caller's.
+void grad_targets(float*& gi, float*& gt, int64_t b, int64_t d, char* ws, const Layout& L) {
+  if (L.dk == d) return;
+  gi = (float*)(ws + L.gpad);
+  gt = gi + b * L.dk;
+}
+bool unstage_grads(float* dimg, float* dtxt, int64_t rows, int64_t b, int64_t d, char* ws, const Layout& L,
+                   hipStream_t stream) {
+  if (L.dk == d) return true;
+  const int cin = (int)(L.dk * 4 / 16), cout = (int)(d * 4 / 16);
+  const uint4* gi = (const uint4*)(ws + L.gpad);
+  const uint4* gt = gi + b * L.dk / 4;
+  const int64_t n = rows * cout;
+  hipLaunchKernelGGL(copy_rows, dim3(copy_grid(n)), dim3(256), 0, stream, gi, (uint4*)dimg, rows, cin, cout);
+  hipLaunchKernelGGL(copy_rows, dim3(copy_grid(n)), dim3(256), 0, stream, gt, (uint4*)dtxt, rows, cin, cout);
+  return hipGetLastError() == hipSuccess;
+}
+
 
 bool aligned(const void* p, size_t a) { return p != nullptr && ((uintptr_t)p % a) == 0; }
 
@@ -81,7 +152,9 @@ bool shape_ok(int64_t b, int64_t d, int dtype) {
   return b >= 1 && d >= 1 && (dtype == INFCL_BF16 || dtype == INFCL_F32 || dtype == INFCL_F16);
 }
 
-bool shape_supported(int64_t b, int64_t d, int dtype) { return b <= kMaxB && infcl::bwd_supported(d, dtype); }
+bool shape_supported(int64_t b, int64_t d, int dtype) {
+  return b <= kMaxB && width_ok(d, dtype) && infcl::bwd_supported(kernel_width(d, dtype), dtype);
+}
 
 // A shard: own samples [r0, r0 + bs) of the batch, r0 a multiple of 32 (so
 // that own row blocks line up with the 32-row swept tiles).
@@ -136,7 +209,8 @@ infcl_status infcl_fwd(const void* img, const void* txt, int64_t b, int64_t d, i
   const Layout L = make_layout(b, d, dtype);
   if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)workspace;
-  int rc = infcl::launch_fwd(img, txt, b, d, dtype, scale, loss, loss64, lse_r, lse_c, aux, (hipStream_t)stream,
+  if (!stage_inputs(img, txt, b, d, dtype, ws, L, (hipStream_t)stream)) return INFCL_ERR_HIP;
+  int rc = infcl::launch_fwd(img, txt, b, L.dk, dtype, scale, loss, loss64, lse_r, lse_c, aux, (hipStream_t)stream,
                              (float*)(ws + L.rowR), (float*)(ws + L.rowL), (float*)(ws + L.colR),
                              (float*)(ws + L.colL), (float*)(ws + L.udiag), (float*)(ws + L.ref2),
                              (double*)(ws + L.fwd_part));
@@ -155,7 +229,8 @@ infcl_status infcl_fwd_noalloc(const void* img, const void* txt, int64_t b, int6
   if (L.total > kScratchBytes) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)scratch_address();
   if (ws == nullptr) return INFCL_ERR_HIP;
-  int rc = infcl::launch_fwd(img, txt, b, d, dtype, scale, loss, loss64, lse_r, lse_c, aux, (hipStream_t)stream,
+  if (!stage_inputs(img, txt, b, d, dtype, ws, L, (hipStream_t)stream)) return INFCL_ERR_HIP;
+  int rc = infcl::launch_fwd(img, txt, b, L.dk, dtype, scale, loss, loss64, lse_r, lse_c, aux, (hipStream_t)stream,
                              (float*)(ws + L.rowR), (float*)(ws + L.rowL), (float*)(ws + L.colR),
                              (float*)(ws + L.colL), (float*)(ws + L.udiag), (float*)(ws + L.ref2),
                              (double*)(ws + L.fwd_part));
@@ -175,10 +250,14 @@ infcl_status infcl_bwd(const void* img, const void* txt, int64_t b, int64_t d, i
   const Layout L = make_layout(b, d, dtype);
   if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)workspace;
-  int rc = infcl::launch_bwd(img, txt, b, d, dtype, 0, b, scale, lse_r, lse_c, aux, dloss, dimg, dtxt, dscale, nullptr,
+  if (!stage_inputs(img, txt, b, d, dtype, ws, L, (hipStream_t)stream)) return INFCL_ERR_HIP;
+  float *gi = dimg, *gt = dtxt;
+  grad_targets(gi, gt, b, d, ws, L);
+  int rc = infcl::launch_bwd(img, txt, b, L.dk, dtype, 0, b, scale, lse_r, lse_c, aux, dloss, gi, gt, dscale, nullptr,
                              (float*)(ws + L.lse2), (double*)(ws + L.bwd_part), (float*)(ws + L.g16),
                              (hipStream_t)stream);
   if (rc == 2) return INFCL_ERR_UNSUPPORTED;
+  if (rc == 0 && !unstage_grads(dimg, dtxt, b, b, d, ws, L, (hipStream_t)stream)) rc = 1;
   return rc == 0 ? INFCL_OK : INFCL_ERR_HIP;
 }
 
@@ -195,7 +274,8 @@ infcl_status infcl_fwd_shard(const void* img, const void* txt, int64_t b, int64_
   const Layout L = make_layout(b, d, dtype);
   if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)workspace;
-  int rc = infcl::launch_fwd_shard(img, txt, b, d, dtype, r0, bs, scale, colpair, (hipStream_t)stream,
+  if (!stage_inputs(img, txt, b, d, dtype, ws, L, (hipStream_t)stream)) return INFCL_ERR_HIP;
+  int rc = infcl::launch_fwd_shard(img, txt, b, L.dk, dtype, r0, bs, scale, colpair, (hipStream_t)stream,
                                    (float*)(ws + L.rowR), (float*)(ws + L.rowL), (float*)(ws + L.colR),
                                    (float*)(ws + L.colL), (float*)(ws + L.udiag), (float*)(ws + L.ref2));
   return rc == 0 ? INFCL_OK : INFCL_ERR_HIP;
@@ -212,7 +292,7 @@ infcl_status infcl_fwd_shard_finish(int64_t b, int64_t d, int dtype, int64_t r0,
   const Layout L = make_layout(b, d, dtype);
   if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)workspace;
-  int rc = infcl::launch_fwd_shard_finish(b, d, dtype, r0, bs, nparts, colpairs, scale, lse_r, lse_c, aux, loss_part,
+  int rc = infcl::launch_fwd_shard_finish(b, L.dk, dtype, r0, bs, nparts, colpairs, scale, lse_r, lse_c, aux, loss_part,
                                           (hipStream_t)stream, (const float*)(ws + L.rowR),
                                           (const float*)(ws + L.rowL), (const float*)(ws + L.udiag),
                                           (double*)(ws + L.fwd_part));
@@ -233,10 +313,14 @@ infcl_status infcl_bwd_shard(const void* img, const void* txt, int64_t b, int64_
   const Layout L = make_layout(b, d, dtype);
   if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)workspace;
-  int rc = infcl::launch_bwd(img, txt, b, d, dtype, r0, bs, scale, lse_r, lse_c, aux, dloss, dimg, dtxt, nullptr,
+  if (!stage_inputs(img, txt, b, d, dtype, ws, L, (hipStream_t)stream)) return INFCL_ERR_HIP;
+  float *gi = dimg, *gt = dtxt;
+  grad_targets(gi, gt, b, d, ws, L);
+  int rc = infcl::launch_bwd(img, txt, b, L.dk, dtype, r0, bs, scale, lse_r, lse_c, aux, dloss, gi, gt, nullptr,
                              dscale_part, (float*)(ws + L.lse2), (double*)(ws + L.bwd_part), (float*)(ws + L.g16),
                              (hipStream_t)stream);
   if (rc == 2) return INFCL_ERR_UNSUPPORTED;
+  if (rc == 0 && !unstage_grads(dimg, dtxt, bs, b, d, ws, L, (hipStream_t)stream)) rc = 1;
   return rc == 0 ? INFCL_OK : INFCL_ERR_HIP;
 }
 
@@ -245,7 +329,7 @@ const char* infcl_status_str(int status) {
     case INFCL_OK: return "ok";
     case INFCL_ERR_INVALID: return "invalid argument (null or misaligned pointer, b < 1, d < 1 or unknown dtype)";
     case INFCL_ERR_UNSUPPORTED:
-      return "unsupported shape (bf16, f16: d in 128..1024 step 128; f32: d in 64..512 step 64; b <= 2^30)";
+      return "unsupported shape (bf16, f16: d a multiple of 8 up to 1024; f32: d a multiple of 4 up to 512; b <= 2^30)";
     case INFCL_ERR_WORKSPACE: return "workspace smaller than infcl_workspace_size()";
     case INFCL_ERR_HIP: return "HIP kernel launch failed";
     default: return "unknown status";

@@ -80,12 +80,30 @@ def test_workspace_bytes_per_sample(d, dt, per_sample):
     (0, 512, 0, infcl.INFCL_ERR_INVALID), (-3, 512, 0, infcl.INFCL_ERR_INVALID), (16, 0, 0, infcl.INFCL_ERR_INVALID),
     (16, 512, 7, infcl.INFCL_ERR_INVALID), (16, 100, 0, infcl.INFCL_ERR_UNSUPPORTED),
     (16, 2048, 0, infcl.INFCL_ERR_UNSUPPORTED), (16, 1024, 1, infcl.INFCL_ERR_UNSUPPORTED),
-    (16, 64, 0, infcl.INFCL_ERR_UNSUPPORTED), (16, 64, 1, infcl.INFCL_OK), ((1 << 30) + 1, 512, 0, infcl.INFCL_ERR_UNSUPPORTED),
-    (16, 512, 2, infcl.INFCL_OK), (16, 1024, 2, infcl.INFCL_OK), (16, 64, 2, infcl.INFCL_ERR_UNSUPPORTED),
+    (16, 64, 0, infcl.INFCL_OK), (16, 64, 1, infcl.INFCL_OK), ((1 << 30) + 1, 512, 0, infcl.INFCL_ERR_UNSUPPORTED),
+    (16, 512, 2, infcl.INFCL_OK), (16, 1024, 2, infcl.INFCL_OK), (16, 64, 2, infcl.INFCL_OK),
     (16, 100, 2, infcl.INFCL_ERR_UNSUPPORTED), (16, 512, 3, infcl.INFCL_ERR_INVALID),
+    # 16-bit: any multiple of 8 up to 1024; f32: any multiple of 4 up to 512
+    (16, 8, 0, infcl.INFCL_OK), (16, 1000, 0, infcl.INFCL_OK), (16, 1020, 0, infcl.INFCL_ERR_UNSUPPORTED),
+    (16, 1032, 0, infcl.INFCL_ERR_UNSUPPORTED), (16, 4, 0, infcl.INFCL_ERR_UNSUPPORTED), (16, 4, 1, infcl.INFCL_OK),
+    (16, 36, 1, infcl.INFCL_OK), (16, 514, 1, infcl.INFCL_ERR_UNSUPPORTED), (16, 516, 1, infcl.INFCL_ERR_UNSUPPORTED),
 ])
 def test_workspace_size_validation(b, d, dt, expect):
     assert _ws(b, d, dt)[0] == expect
+
+
+@pytest.mark.parametrize("d,dt,dk,es", [(8, 0, 128, 2), (72, 0, 128, 2), (200, 2, 256, 2), (1000, 0, 1024, 2),
+                                         (4, 1, 64, 4), (100, 1, 128, 4)])
+def test_workspace_of_padded_widths(d, dt, dk, es):
+    """A width the sweeps are not built for runs at the next multiple of 128
+    (16-bit) or 64 (f32): the workspace is that of the padded width plus the
+    zero-padded copies of both inputs and the padded fp32 gradients."""
+    b = 1 << 16
+    st, w = _ws(b, d, dt)
+    st_k, w_k = _ws(b, dk, dt)
+    assert st == st_k == infcl.INFCL_OK
+    extra = 2 * b * dk * es + 2 * b * dk * 4
+    assert w_k + extra <= w <= w_k + extra + 1024
 
 
 def test_workspace_size_null_out(lib):
@@ -109,7 +127,8 @@ def _bwd(lib, img=A, txt=A, b=64, d=512, dt=0, scale=A, lr=A, lc=A, aux=A, dloss
     (dict(loss64=A + 4), infcl.INFCL_ERR_INVALID), (dict(lr=A + 4), infcl.INFCL_ERR_INVALID),
     (dict(aux=None), infcl.INFCL_ERR_INVALID), (dict(ws=A + 16), infcl.INFCL_ERR_INVALID),
     (dict(b=0), infcl.INFCL_ERR_INVALID), (dict(d=-1), infcl.INFCL_ERR_INVALID), (dict(dt=3), infcl.INFCL_ERR_INVALID),
-    (dict(d=96), infcl.INFCL_ERR_UNSUPPORTED), (dict(wsb=16), infcl.INFCL_ERR_WORKSPACE),
+    (dict(d=100), infcl.INFCL_ERR_UNSUPPORTED), (dict(wsb=16), infcl.INFCL_ERR_WORKSPACE),
+    (dict(d=96, wsb=16), infcl.INFCL_ERR_WORKSPACE),
 ])
 def test_fwd_validation(lib, kw, expect):
     assert _fwd(lib, **kw) == expect
@@ -124,7 +143,7 @@ def _fwd_noalloc(lib, img=A, txt=A, b=64, d=512, dt=0, scale=A, loss=A, loss64=A
     (dict(scale=None), infcl.INFCL_ERR_INVALID), (dict(loss=None), infcl.INFCL_ERR_INVALID),
     (dict(loss64=A + 4), infcl.INFCL_ERR_INVALID), (dict(lc=A + 4), infcl.INFCL_ERR_INVALID),
     (dict(b=0), infcl.INFCL_ERR_INVALID), (dict(dt=3), infcl.INFCL_ERR_INVALID),
-    (dict(d=96), infcl.INFCL_ERR_UNSUPPORTED),
+    (dict(d=100), infcl.INFCL_ERR_UNSUPPORTED),
     # the fixed 32 MiB scratch: 16-bit inputs need 336 B per sample, f32 780 B
     (dict(b=100000), infcl.INFCL_ERR_WORKSPACE), (dict(b=50000, d=256, dt=1), infcl.INFCL_ERR_WORKSPACE),
 ])
@@ -161,7 +180,7 @@ def _bwd_shard(lib, b=1000, d=512, dt=0, r0=0, bs=1000, ds=A, di=A, wsb=1 << 30)
 @pytest.mark.parametrize("kw,expect", [
     (dict(r0=16), infcl.INFCL_ERR_INVALID), (dict(r0=-32), infcl.INFCL_ERR_INVALID), (dict(bs=0), infcl.INFCL_ERR_INVALID),
     (dict(r0=992, bs=9), infcl.INFCL_ERR_INVALID), (dict(cp=A + 4), infcl.INFCL_ERR_INVALID),
-    (dict(cp=None), infcl.INFCL_ERR_INVALID), (dict(d=96), infcl.INFCL_ERR_UNSUPPORTED),
+    (dict(cp=None), infcl.INFCL_ERR_INVALID), (dict(d=100), infcl.INFCL_ERR_UNSUPPORTED),
     (dict(wsb=16), infcl.INFCL_ERR_WORKSPACE),
 ])
 def test_fwd_shard_validation(lib, kw, expect):

@@ -146,23 +146,34 @@ def test_config1_fp32_workload():
     _check(gpu, fwd, dI, dT, ds, s, c["d"], "f32")
 
 
-@pytest.mark.parametrize("d", [8, 72, 200, 1000])
-def test_zero_padded_features_bf16(d):
-    """16-bit widths that are not a multiple of 128 are run by padding the
-    features with zeros up to the next multiple: zero features add nothing to
-    any dot product, so loss, r, c and dscale are those of the unpadded batch,
-    the gradients' first d columns are its gradients and the padding columns'
-    gradients are exactly zero.  Checked against the oracle at the unpadded d."""
+@pytest.mark.parametrize("d,dtype", [(8, "bf16"), (72, "bf16"), (200, "bf16"), (1000, "bf16"), (24, "f16"),
+                                     (520, "f16"), (4, "f32"), (36, "f32"), (100, "f32"), (500, "f32")])
+def test_widths_between_kernel_widths(d, dtype):
+    """Widths the sweeps are not built for (16-bit: not a multiple of 128; f32:
+    not a multiple of 64) go through the C ABI as they are: the library runs
+    the sweeps on zero-padded copies and drops the padding's gradients.  Zero
+    features add nothing to any dot product, so the results are those of the
+    unpadded batch (checked against the oracle at d) and, bit for bit, those
+    of the same inputs padded by the caller (the same kernels on the same
+    values)."""
     b = 513
-    img, txt = synth.clip_pairs(b, d, 1.0, seed=d, dtype="bf16")
-    dp = -(-d // 128) * 128
-    pi = np.zeros((b, dp), dtype=np.uint16)
-    pt = np.zeros((b, dp), dtype=np.uint16)
+    img, txt = synth.clip_pairs(b, d, 1.0, seed=d, dtype=dtype)
+    s = f32_scale(14.29)
+    gpu = run(img, txt, dtype, s)
+    fwd, dI, dT, ds = oracle.forward_backward(synth.as_f64(img, dtype), synth.as_f64(txt, dtype), s)
+    assert gpu["dI"].shape == (b, d) and gpu["dT"].shape == (b, d)
+    _check(gpu, fwd, dI, dT, ds, s, d, dtype)
+    q = 64 if dtype == "f32" else 128
+    dp = -(-d // q) * q
+    pi = np.zeros((b, dp), dtype=img.dtype)
+    pt = np.zeros((b, dp), dtype=txt.dtype)
     pi[:, :d] = img
     pt[:, :d] = txt
-    s = f32_scale(14.29)
-    gpu = run(pi, pt, "bf16", s)
-    fwd, dI, dT, ds = oracle.forward_backward(synth.as_f64(img, "bf16"), synth.as_f64(txt, "bf16"), s)
-    assert np.all(gpu["dI"][:, d:] == 0) and np.all(gpu["dT"][:, d:] == 0)
-    gpu["dI"], gpu["dT"] = gpu["dI"][:, :d], gpu["dT"][:, :d]
-    _check(gpu, fwd, dI, dT, ds, s, d, "bf16")
+    padded = run(pi, pt, dtype, s)
+    assert np.all(padded["dI"][:, d:] == 0) and np.all(padded["dT"][:, d:] == 0)
+    for k in ("loss64", "loss", "dscale"):
+        assert gpu[k] == padded[k], k
+    for k in ("lse_r", "lse_c", "ell_r", "ell_c", "u_diag"):
+        np.testing.assert_array_equal(gpu[k], padded[k], err_msg=k)
+    np.testing.assert_array_equal(gpu["dI"], padded["dI"][:, :d])
+    np.testing.assert_array_equal(gpu["dT"], padded["dT"][:, :d])

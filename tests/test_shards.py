@@ -43,6 +43,7 @@ def _sharded(img, txt, dtype, s, n, dloss=1.0):
     (1025, 128, "f32", 3),     # fp32 inputs
     (1500, 512, "f16", 5),     # fp16 inputs
     (300, 128, "bf16", 10),    # shards of 32 rows and a ragged last one of 12
+    (700, 200, "bf16", 3),     # a width the sweeps run zero-padded (256)
 ])
 def test_sharded_matches_oracle_and_whole_batch(b, d, dtype, n):
     img, txt = synth.clip_pairs(b, d, 1.0, seed=b + n, dtype=dtype)
