@@ -27,7 +27,8 @@ def _np(o):
     return {k: v.cpu().numpy() for k, v in o.items()}
 
 
-@pytest.mark.parametrize("d,dtype", [(512, "bf16"), (768, "bf16"), (256, "f32")])
+@pytest.mark.parametrize("d,dtype", [(512, "bf16"), (768, "bf16"), (256, "f32"),
+                                     (200, "bf16"), (100, "f32")])  # run zero-padded in the scratch
 def test_noalloc_forward_matches_workspace_forward(d, dtype):
     s = f32_scale(14.29)
     for b in (5000, 1337):  # the second call is smaller
