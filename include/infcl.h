@@ -71,8 +71,8 @@ typedef enum { INFCL_BF16 = 0, INFCL_F32 = 1, INFCL_F16 = 2 } infcl_dtype;
 /* Bytes of device workspace that infcl_fwd / infcl_bwd need for (b, d, dtype).
  * The same workspace size serves both calls.  It is linear in b: a few
  * vectors of b floats, plus, when d is not a multiple of 128 (16-bit) or 64
- * (f32), the padded copies of img and txt and the padded fp32 gradients
- * (2 b d' elements each, d' the padded width).  Returns INFCL_ERR_INVALID for
+ * (f32), the padded copies of img and txt and the padded gradients
+ * (2 b d' fp32 elements, d' the padded width).  Returns INFCL_ERR_INVALID for
  * a NULL `bytes` or b < 1, d < 1 or an unknown dtype. */
 infcl_status infcl_workspace_size(int64_t b, int64_t d, int dtype, size_t* bytes);
 
@@ -95,16 +95,20 @@ infcl_status infcl_fwd(const void* img, const void* txt, int64_t b, int64_t d, i
 
 /* Backward pass (Eq. 6-8 completed for both halves, the text side and the
  * scale; the appendix's in-GPU backward algorithm with recomputed tiles):
- *   dimg  [b, d] float   dloss * dL/dimg
- *   dtxt  [b, d] float   dloss * dL/dtxt
- *   dscale [1] float     dloss * dL/ds (derivative w.r.t. s itself)
- * dloss is a device pointer to one float (NULL means 1).  lse_r, lse_c and aux
- * must come from infcl_fwd on the same inputs.  Two sweeps run: one owns rows
- * of img and accumulates dimg in registers, the other owns rows of txt; the
- * softmax is never written to memory. */
+ *   dimg  [b, d] grad_dtype  dloss * dL/dimg
+ *   dtxt  [b, d] grad_dtype  dloss * dL/dtxt
+ *   dscale [1] float         dloss * dL/ds (derivative w.r.t. s itself)
+ * grad_dtype: INFCL_F32, or for 16-bit inputs also their own type (bf16
+ * gradients of bf16 inputs, f16 of f16): the gradients accumulate in fp32 and
+ * are rounded once, to nearest even, when stored.  Another known type returns
+ * INFCL_ERR_UNSUPPORTED, an unknown one INFCL_ERR_INVALID.  dloss is a device
+ * pointer to one float (NULL means 1).  lse_r, lse_c and aux must come from
+ * infcl_fwd on the same inputs.  Two sweeps run: one owns rows of img and
+ * accumulates dimg in registers, the other owns rows of txt; the softmax is
+ * never written to memory. */
 infcl_status infcl_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype,
                        const float* scale, const float* lse_r, const float* lse_c, const float* aux,
-                       const float* dloss, float* dimg, float* dtxt, float* dscale,
+                       const float* dloss, void* dimg, void* dtxt, int grad_dtype, float* dscale,
                        void* workspace, size_t ws_bytes, void* stream);
 
 /* ---- One GPU's share of a batch sharded over n GPUs (Sec. 3.2, cross-GPU
@@ -152,12 +156,12 @@ infcl_status infcl_fwd_shard_finish(int64_t b, int64_t d, int dtype, int64_t r0,
 
 /* Step 5.  lse_r, lse_c [b] and aux [3b] cover all b samples (the all-gather
  * of every shard's finish outputs, in sample order).  Outputs (device):
- * dimg, dtxt [bs, d] float, the gradients of own samples, and
- * dscale_part [1] double, this shard's share of dloss * dL/ds. */
+ * dimg, dtxt [bs, d] of grad_dtype (as in infcl_bwd), the gradients of own
+ * samples, and dscale_part [1] double, this shard's share of dloss * dL/ds. */
 infcl_status infcl_bwd_shard(const void* img, const void* txt, int64_t b, int64_t d, int dtype,
                              int64_t r0, int64_t bs, const float* scale, const float* lse_r,
                              const float* lse_c, const float* aux, const float* dloss,
-                             float* dimg, float* dtxt, double* dscale_part,
+                             void* dimg, void* dtxt, int grad_dtype, double* dscale_part,
                              void* workspace, size_t ws_bytes, void* stream);
 
 /* For callers that cannot allocate device memory (code under HIP graph

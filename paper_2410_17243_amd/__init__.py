@@ -10,9 +10,10 @@ Entry points with the C ABI's names (tensors in, status checked):
     infcl_fwd(img, txt, scale, loss, loss64, lse_r, lse_c, aux, workspace)
     infcl_fwd_noalloc(img, txt, scale, loss, loss64, lse_r, lse_c, aux)
     infcl_bwd(img, txt, scale, lse_r, lse_c, aux, dloss, dimg, dtxt, dscale, workspace)
+        (the gradient type passed to the C call is dimg's dtype)
 Convenience wrappers that allocate outputs with torch:
     clip_loss_fwd(img, txt, scale) -> dict
-    clip_loss_bwd(img, txt, scale, fwd, dloss=None) -> (dimg, dtxt, dscale)
+    clip_loss_bwd(img, txt, scale, fwd, dloss=None, grad_dtype=None) -> (dimg, dtxt, dscale)
     clip_loss(img, txt, scale) -> loss   (torch.autograd.Function)
 """
 
@@ -58,13 +59,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.infcl_fwd.restype = ip
     lib.infcl_fwd_noalloc.argtypes = [vp, vp, i64, i64, ip, vp, vp, vp, vp, vp, vp, vp]
     lib.infcl_fwd_noalloc.restype = ip
-    lib.infcl_bwd.argtypes = [vp, vp, i64, i64, ip, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.infcl_bwd.argtypes = [vp, vp, i64, i64, ip, vp, vp, vp, vp, vp, vp, vp, ip, vp, vp, sz, vp]
     lib.infcl_bwd.restype = ip
     lib.infcl_fwd_shard.argtypes = [vp, vp, i64, i64, ip, i64, i64, vp, vp, vp, sz, vp]
     lib.infcl_fwd_shard.restype = ip
     lib.infcl_fwd_shard_finish.argtypes = [i64, i64, ip, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.infcl_fwd_shard_finish.restype = ip
-    lib.infcl_bwd_shard.argtypes = [vp, vp, i64, i64, ip, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.infcl_bwd_shard.argtypes = [vp, vp, i64, i64, ip, i64, i64, vp, vp, vp, vp, vp, vp, vp, ip, vp, vp, sz, vp]
     lib.infcl_bwd_shard.restype = ip
     lib.infcl_ablation_bwd_single.argtypes = [vp, vp, i64, i64, ip, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.infcl_ablation_bwd_single.restype = ip
@@ -137,9 +138,9 @@ def infcl_fwd_noalloc(img, txt, scale, loss, loss64, lse_r, lse_c, aux):
 def infcl_bwd(img, txt, scale, lse_r, lse_c, aux, dloss, dimg, dtxt, dscale, workspace):
     b, d = img.shape
     _check(load_library().infcl_bwd(_ptr(img), _ptr(txt), b, d, _dtype_code(img), _ptr(scale), _ptr(lse_r),
-                                     _ptr(lse_c), _ptr(aux), _ptr(dloss), _ptr(dimg), _ptr(dtxt), _ptr(dscale),
-                                     _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(img)),
-           "infcl_bwd")
+                                     _ptr(lse_c), _ptr(aux), _ptr(dloss), _ptr(dimg), _ptr(dtxt), _dtype_code(dimg),
+                                     _ptr(dscale), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                     _stream(img)), "infcl_bwd")
 
 
 def infcl_fwd_shard(img, txt, scale, r0, bs, colpair, workspace):
@@ -162,7 +163,7 @@ def infcl_bwd_shard(img, txt, scale, r0, bs, lse_r, lse_c, aux, dloss, dimg, dtx
     b, d = img.shape
     _check(load_library().infcl_bwd_shard(_ptr(img), _ptr(txt), b, d, _dtype_code(img), int(r0), int(bs), _ptr(scale),
                                            _ptr(lse_r), _ptr(lse_c), _ptr(aux), _ptr(dloss), _ptr(dimg), _ptr(dtxt),
-                                           _ptr(dscale_part), _ptr(workspace),
+                                           _dtype_code(dimg), _ptr(dscale_part), _ptr(workspace),
                                            workspace.numel() * workspace.element_size(), _stream(img)),
            "infcl_bwd_shard")
 
@@ -237,7 +238,9 @@ def clip_loss_fwd(img, txt, scale, workspace=None) -> dict:
     return out
 
 
-def clip_loss_bwd(img, txt, scale, fwd: dict, dloss=None, workspace=None):
+def clip_loss_bwd(img, txt, scale, fwd: dict, dloss=None, workspace=None, grad_dtype=None):
+    """dimg, dtxt and dscale.  grad_dtype: torch.float32 (default), or the
+    inputs' own 16-bit dtype (rounded once from the fp32 accumulators)."""
     import torch
 
     _validate(img, txt, scale)
@@ -246,8 +249,11 @@ def clip_loss_bwd(img, txt, scale, fwd: dict, dloss=None, workspace=None):
     _check_vec(fwd["lse_r"], b, "lse_r", dev)
     _check_vec(fwd["lse_c"], b, "lse_c", dev)
     _check_vec(fwd["aux"], 3 * b, "aux", dev)
-    dimg = torch.empty((b, d), dtype=torch.float32, device=img.device)
-    dtxt = torch.empty((b, d), dtype=torch.float32, device=img.device)
+    gdt = torch.float32 if grad_dtype is None else grad_dtype
+    if gdt not in (torch.float32, img.dtype):
+        raise TypeError(f"grad_dtype must be float32 or the inputs' dtype {img.dtype}, got {gdt}")
+    dimg = torch.empty((b, d), dtype=gdt, device=img.device)
+    dtxt = torch.empty((b, d), dtype=gdt, device=img.device)
     dscale = torch.empty((), dtype=torch.float32, device=img.device)
     ws = workspace if workspace is not None else fwd.get("workspace")
     if ws is None:
@@ -276,8 +282,11 @@ def _make_function():
         def backward(ctx, dloss):
             img, txt, scale, lse_r, lse_c, aux = ctx.saved_tensors
             fwd = {"lse_r": lse_r, "lse_c": lse_c, "aux": aux}
-            dimg, dtxt, dscale = clip_loss_bwd(img, txt, scale, fwd, dloss=dloss, workspace=ctx.ws)
-            return dimg.to(img.dtype), dtxt.to(txt.dtype), dscale.reshape(scale.shape)
+            # gradients in the inputs' dtype straight from the kernels (one
+            # rounding of the fp32 accumulators, as a cast would do)
+            dimg, dtxt, dscale = clip_loss_bwd(img, txt, scale, fwd, dloss=dloss, workspace=ctx.ws,
+                                               grad_dtype=img.dtype)
+            return dimg, dtxt, dscale.reshape(scale.shape)
 
     return ClipLoss
 

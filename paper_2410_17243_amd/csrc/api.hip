@@ -24,8 +24,8 @@ void fwd2_grid(int64_t b, int64_t nrows, int64_t d, int* Pr, int* Pc);
 bool fwd2_supported(int64_t d, int dtype);
 int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, int64_t r0, int64_t nrows,
                const float* scale, const float* lse_r, const float* lse_c, const float* aux, const float* dloss,
-               float* dimg, float* dtxt, float* dscale, double* dscale64, float* lse2, double* ds_part, float* g16,
-               hipStream_t stream);
+               void* dimg, void* dtxt, int gdt, float* dscale, double* dscale64, float* lse2, double* ds_part,
+               float* g16, hipStream_t stream);
 bool bwd_supported(int64_t d, int dtype);
 }  // namespace infcl
 
@@ -125,20 +125,29 @@ bool stage_inputs(const void*& img, const void*& txt, int64_t b, int64_t d, int 
   return true;
 }
 
+// Gradient element type: 0 fp32, 1 the 16-bit input type; -1 for an unknown
+// type, -2 for a known one that is neither (16-bit gradients of another type,
+// or of fp32 inputs, are not built).
+int grad_kind(int grad_dtype, int dtype) {
+  if (grad_dtype != INFCL_BF16 && grad_dtype != INFCL_F32 && grad_dtype != INFCL_F16) return -1;
+  if (grad_dtype == INFCL_F32) return 0;
+  return grad_dtype == dtype ? 1 : -2;
+}
+
 // Where the sweeps write the gradients of `rows` own samples: the caller's
 // dimg and dtxt, or padded buffers in the workspace that unstage_grads then
-// copies, without the padding, into the caller's.
-void grad_targets(float*& gi, float*& gt, int64_t b, int64_t d, char* ws, const Layout& L) {
+// copies, without the padding, into the caller's.  ges: gradient element size.
+void grad_targets(void*& gi, void*& gt, int64_t b, int64_t d, size_t ges, char* ws, const Layout& L) {
   if (L.dk == d) return;
-  gi = (float*)(ws + L.gpad);
-  gt = gi + b * L.dk;
+  gi = ws + L.gpad;
+  gt = ws + L.gpad + (size_t)b * (size_t)L.dk * ges;
 }
-bool unstage_grads(float* dimg, float* dtxt, int64_t rows, int64_t b, int64_t d, char* ws, const Layout& L,
-                   hipStream_t stream) {
+bool unstage_grads(void* dimg, void* dtxt, int64_t rows, int64_t b, int64_t d, size_t ges, char* ws,
+                   const Layout& L, hipStream_t stream) {
   if (L.dk == d) return true;
-  const int cin = (int)(L.dk * 4 / 16), cout = (int)(d * 4 / 16);
+  const int cin = (int)(L.dk * ges / 16), cout = (int)(d * ges / 16);
   const uint4* gi = (const uint4*)(ws + L.gpad);
-  const uint4* gt = gi + b * L.dk / 4;
+  const uint4* gt = gi + b * cin;
   const int64_t n = rows * cout;
   hipLaunchKernelGGL(copy_rows, dim3(copy_grid(n)), dim3(256), 0, stream, gi, (uint4*)dimg, rows, cin, cout);
   hipLaunchKernelGGL(copy_rows, dim3(copy_grid(n)), dim3(256), 0, stream, gt, (uint4*)dtxt, rows, cin, cout);
@@ -238,26 +247,28 @@ infcl_status infcl_fwd_noalloc(const void* img, const void* txt, int64_t b, int6
 }
 
 infcl_status infcl_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, const float* scale,
-                       const float* lse_r, const float* lse_c, const float* aux, const float* dloss, float* dimg,
-                       float* dtxt, float* dscale, void* workspace, size_t ws_bytes, void* stream) {
-  if (!shape_ok(b, d, dtype)) return INFCL_ERR_INVALID;
+                       const float* lse_r, const float* lse_c, const float* aux, const float* dloss, void* dimg,
+                       void* dtxt, int grad_dtype, float* dscale, void* workspace, size_t ws_bytes, void* stream) {
+  const int gk = grad_kind(grad_dtype, dtype);
+  if (!shape_ok(b, d, dtype) || gk == -1) return INFCL_ERR_INVALID;
   if (!aligned(img, 16) || !aligned(txt, 16) || !aligned(scale, 4) || !aligned(lse_r, 16) || !aligned(lse_c, 16) ||
       !aligned(aux, 16) || !aligned(dimg, 16) || !aligned(dtxt, 16) || !aligned(dscale, 4) ||
       !aligned(workspace, 256))
     return INFCL_ERR_INVALID;
   if (dloss != nullptr && ((uintptr_t)dloss % 4) != 0) return INFCL_ERR_INVALID;
-  if (!shape_supported(b, d, dtype)) return INFCL_ERR_UNSUPPORTED;
+  if (!shape_supported(b, d, dtype) || gk < 0) return INFCL_ERR_UNSUPPORTED;
   const Layout L = make_layout(b, d, dtype);
   if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)workspace;
   if (!stage_inputs(img, txt, b, d, dtype, ws, L, (hipStream_t)stream)) return INFCL_ERR_HIP;
-  float *gi = dimg, *gt = dtxt;
-  grad_targets(gi, gt, b, d, ws, L);
-  int rc = infcl::launch_bwd(img, txt, b, L.dk, dtype, 0, b, scale, lse_r, lse_c, aux, dloss, gi, gt, dscale, nullptr,
-                             (float*)(ws + L.lse2), (double*)(ws + L.bwd_part), (float*)(ws + L.g16),
+  const size_t ges = gk ? 2 : 4;
+  void *gi = dimg, *gt = dtxt;
+  grad_targets(gi, gt, b, d, ges, ws, L);
+  int rc = infcl::launch_bwd(img, txt, b, L.dk, dtype, 0, b, scale, lse_r, lse_c, aux, dloss, gi, gt, gk, dscale,
+                             nullptr, (float*)(ws + L.lse2), (double*)(ws + L.bwd_part), (float*)(ws + L.g16),
                              (hipStream_t)stream);
   if (rc == 2) return INFCL_ERR_UNSUPPORTED;
-  if (rc == 0 && !unstage_grads(dimg, dtxt, b, b, d, ws, L, (hipStream_t)stream)) rc = 1;
+  if (rc == 0 && !unstage_grads(dimg, dtxt, b, b, d, ges, ws, L, (hipStream_t)stream)) rc = 1;
   return rc == 0 ? INFCL_OK : INFCL_ERR_HIP;
 }
 
@@ -301,26 +312,28 @@ infcl_status infcl_fwd_shard_finish(int64_t b, int64_t d, int dtype, int64_t r0,
 
 infcl_status infcl_bwd_shard(const void* img, const void* txt, int64_t b, int64_t d, int dtype, int64_t r0,
                              int64_t bs, const float* scale, const float* lse_r, const float* lse_c, const float* aux,
-                             const float* dloss, float* dimg, float* dtxt, double* dscale_part, void* workspace,
-                             size_t ws_bytes, void* stream) {
-  if (!shape_ok(b, d, dtype) || !shard_ok(b, r0, bs)) return INFCL_ERR_INVALID;
+                             const float* dloss, void* dimg, void* dtxt, int grad_dtype, double* dscale_part,
+                             void* workspace, size_t ws_bytes, void* stream) {
+  const int gk = grad_kind(grad_dtype, dtype);
+  if (!shape_ok(b, d, dtype) || !shard_ok(b, r0, bs) || gk == -1) return INFCL_ERR_INVALID;
   if (!aligned(img, 16) || !aligned(txt, 16) || !aligned(scale, 4) || !aligned(lse_r, 16) || !aligned(lse_c, 16) ||
       !aligned(aux, 16) || !aligned(dimg, 16) || !aligned(dtxt, 16) || !aligned(dscale_part, 8) ||
       !aligned(workspace, 256))
     return INFCL_ERR_INVALID;
   if (dloss != nullptr && ((uintptr_t)dloss % 4) != 0) return INFCL_ERR_INVALID;
-  if (!shape_supported(b, d, dtype)) return INFCL_ERR_UNSUPPORTED;
+  if (!shape_supported(b, d, dtype) || gk < 0) return INFCL_ERR_UNSUPPORTED;
   const Layout L = make_layout(b, d, dtype);
   if (ws_bytes < L.total) return INFCL_ERR_WORKSPACE;
   char* ws = (char*)workspace;
   if (!stage_inputs(img, txt, b, d, dtype, ws, L, (hipStream_t)stream)) return INFCL_ERR_HIP;
-  float *gi = dimg, *gt = dtxt;
-  grad_targets(gi, gt, b, d, ws, L);
-  int rc = infcl::launch_bwd(img, txt, b, L.dk, dtype, r0, bs, scale, lse_r, lse_c, aux, dloss, gi, gt, nullptr,
+  const size_t ges = gk ? 2 : 4;
+  void *gi = dimg, *gt = dtxt;
+  grad_targets(gi, gt, b, d, ges, ws, L);
+  int rc = infcl::launch_bwd(img, txt, b, L.dk, dtype, r0, bs, scale, lse_r, lse_c, aux, dloss, gi, gt, gk, nullptr,
                              dscale_part, (float*)(ws + L.lse2), (double*)(ws + L.bwd_part), (float*)(ws + L.g16),
                              (hipStream_t)stream);
   if (rc == 2) return INFCL_ERR_UNSUPPORTED;
-  if (rc == 0 && !unstage_grads(dimg, dtxt, bs, b, d, ws, L, (hipStream_t)stream)) rc = 1;
+  if (rc == 0 && !unstage_grads(dimg, dtxt, bs, b, d, ges, ws, L, (hipStream_t)stream)) rc = 1;
   return rc == 0 ? INFCL_OK : INFCL_ERR_HIP;
 }
 
@@ -329,7 +342,8 @@ const char* infcl_status_str(int status) {
     case INFCL_OK: return "ok";
     case INFCL_ERR_INVALID: return "invalid argument (null or misaligned pointer, b < 1, d < 1 or unknown dtype)";
     case INFCL_ERR_UNSUPPORTED:
-      return "unsupported shape (bf16, f16: d a multiple of 8 up to 1024; f32: d a multiple of 4 up to 512; b <= 2^30)";
+      return "unsupported shape (bf16, f16: d a multiple of 8 up to 1024; f32: d a multiple of 4 up to 512; "
+             "b <= 2^30) or gradient type (f32, or the inputs' 16-bit type)";
     case INFCL_ERR_WORKSPACE: return "workspace smaller than infcl_workspace_size()";
     case INFCL_ERR_HIP: return "HIP kernel launch failed";
     default: return "unknown status";

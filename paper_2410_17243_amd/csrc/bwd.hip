@@ -49,10 +49,12 @@ constexpr int kGpBytes = kBwdBM * kBwdBN * 2;  // one 16-bit G' exchange buffer
 #define INFCL_BWD_G1_PRE 4
 #endif
 
-template <typename TIN, int D, int FB, bool PIPE>
+template <typename TIN, int D, int FB, bool PIPE, bool G16>
 __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
   constexpr int ES = sizeof(TIN);
   constexpr bool F16 = std::is_same<TIN, _Float16>::value;  // fp16 (else bf16) when ES == 2
+  static_assert(ES == 2 || !G16, "16-bit gradients come with 16-bit inputs");
+  using GO = GradOut<G16, F16>;  // gradient element type
   constexpr int KS = D / 16;            // 16-wide contraction steps of GEMM1
   constexpr int ROWG = D * ES;          // bytes per row in HBM
   constexpr int TILEB = kBwdBN * ROWG;  // bytes per swept tile
@@ -499,23 +501,23 @@ __global__ void __launch_bounds__(256, 1) bwd_sweep(BwdParams p) {
       const bool all_ok = wg0 + kBwdBM <= p.own_end;
 #pragma unroll
       for (int ob = 0; ob < 4; ++ob) {
-        float* dst = p.dOwn + (wg0 - p.own_off + 32 * ob + 4 * h) * D + 32 * (pass * FB + wave * FBW) + l32;
+        auto* dst = (typename GO::type*)p.dOwn + (wg0 - p.own_off + 32 * ob + 4 * h) * D + 32 * (pass * FB + wave * FBW) + l32;
 #pragma unroll
         for (int fbw = 0; fbw < FBW; ++fbw)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int64_t row = wg0 + 32 * ob + 8 * (r >> 2) + 4 * h + (r & 3);
-            if (all_ok || row < p.own_end) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fbw] = kfin * dacc[ob * FBW + fbw][r];
+            if (all_ok || row < p.own_end) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fbw] = GO::cvt(kfin * dacc[ob * FBW + fbw][r]);
           }
       }
     } else {
-      float* dst = p.dOwn + (own0 - p.own_off + 4 * h) * D + 32 * pass * FB + l32;
+      auto* dst = (typename GO::type*)p.dOwn + (own0 - p.own_off + 4 * h) * D + 32 * pass * FB + l32;
 #pragma unroll
       for (int fb = 0; fb < FB; ++fb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int64_t row = own0 + 8 * (r >> 2) + 4 * h + (r & 3);
-          if (wave_rows_ok || row < p.own_end) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fb] = kfin * dacc[fb][r];
+          if (wave_rows_ok || row < p.own_end) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fb] = GO::cvt(kfin * dacc[fb][r]);
         }
     }
     // the next pass reuses the tile buffers
@@ -581,7 +583,13 @@ static int launch_bwd_d(const BwdParams& p, int nwg, hipStream_t stream) {
   static_assert(ES == 4 || FB % 4 == 0, "16-bit pass width must be a multiple of 128 features");
   constexpr int TILEB = kBwdBN * D * ES;
   constexpr bool PIPE = INFCL_BWD_PIPE != 0 && ES == 2 && 3 * (TILEB + 128) + 2 * kGpBytes + 2048 <= 160 * 1024;
-  hipLaunchKernelGGL((bwd_sweep<TIN, D, FB, PIPE>), dim3(nwg), dim3(256), 0, stream, p);
+  if constexpr (ES == 2) {
+    if (p.gdt) {
+      hipLaunchKernelGGL((bwd_sweep<TIN, D, FB, PIPE, true>), dim3(nwg), dim3(256), 0, stream, p);
+      return hipGetLastError() == hipSuccess ? 0 : 1;
+    }
+  }
+  hipLaunchKernelGGL((bwd_sweep<TIN, D, FB, PIPE, false>), dim3(nwg), dim3(256), 0, stream, p);
   return hipGetLastError() == hipSuccess ? 0 : 1;
 }
 
@@ -690,13 +698,14 @@ int launch_bwd_wide(const BwdParams& p, int nwg, bool f16, hipStream_t stream);
 // Backward: 16-bit inputs with d = 768 or 1024 take the single-pass wide-row sweep
 // (64 own rows per workgroup), everything else the 128-row sweep above.  Own
 // rows are [r0, r0 + nrows) of both sides (all b for the whole batch; a
-// shard's samples otherwise, with dimg/dtxt [nrows, d]); lse_r, lse_c and aux
-// cover all b samples.  dscale (fp32) and/or dscale64 (fp64) receive this
-// call's share, dloss/(2b) times its partial sums.
+// shard's samples otherwise, with dimg/dtxt [nrows, d]: fp32, or with gdt = 1
+// the 16-bit input type); lse_r, lse_c and aux cover all b samples.  dscale
+// (fp32) and/or dscale64 (fp64) receive this call's share, dloss/(2b) times its
+// partial sums.
 int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype, int64_t r0, int64_t nrows,
                const float* scale, const float* lse_r, const float* lse_c, const float* aux, const float* dloss,
-               float* dimg, float* dtxt, float* dscale, double* dscale64, float* lse2, double* ds_part, float* g16,
-               hipStream_t stream) {
+               void* dimg, void* dtxt, int gdt, float* dscale, double* dscale64, float* lse2, double* ds_part,
+               float* g16, hipStream_t stream) {
   const bool wide = bwd_wide_supported(d, dtype);
   const int nwg = wide ? bwd_wide_workgroups(nrows) : (int)((nrows + kBwdBM - 1) / kBwdBM);
   auto launch = [&](const BwdParams& q) {
@@ -724,6 +733,7 @@ int launch_bwd(const void* img, const void* txt, int64_t b, int64_t d, int dtype
   p.dloss = dloss;
   p.own_off = r0;
   p.own_end = r0 + nrows;
+  p.gdt = gdt;
   // launch 1: own = image rows (dimg), swept = text rows
   p.own = img;
   p.swept = txt;

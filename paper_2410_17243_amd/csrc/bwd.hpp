@@ -17,11 +17,27 @@ struct BwdParams {
   const float* udiag;       // [b]  <img_i, txt_i>
   const float* dloss;       // device scalar or nullptr (= 1)
   int64_t own_off, own_end;  // own rows [own_off, own_end) (a shard; 0 and b for the whole batch)
-  float* dOwn;              // [own_end - own_off, d], by own row - own_off
+  void* dOwn;               // [own_end - own_off, d], by own row - own_off: fp32, or with gdt = 1 the
+                            // input's 16-bit type
   double* ds_part;          // [gridDim.x]
   const float* g16;         // fp16 inputs: (alpha, 1/alpha), the power of two G' is scaled by
+  int gdt;                  // gradient type, which chooses the kernel instantiation: 0 fp32, 1 16-bit
 };
 
 constexpr int kBwdBN = kSweepBN;  // swept rows per tile
+
+// Gradient element type of a sweep: fp32, or with G16 the 16-bit input type
+// (fp16 with F16, else bf16), rounded to nearest even from the fp32
+// accumulator once, when stored.
+template <bool G16, bool F16>
+struct GradOut {
+  using type = float;
+  static __device__ __forceinline__ float cvt(float v) { return v; }
+};
+template <bool F16>
+struct GradOut<true, F16> {
+  using type = __bf16;
+  static __device__ __forceinline__ __bf16 cvt(float v) { return to16<F16>(v); }
+};
 
 }  // namespace infcl

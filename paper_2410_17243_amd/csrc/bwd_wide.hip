@@ -27,6 +27,8 @@
 //           features of the tile (transposing LDS reads), accumulating in
 //           AGPRs.
 // Three barriers per tile (join, G' block, buffer turn-over).
+#include <type_traits>
+
 #include "bwd.hpp"
 
 
@@ -34,8 +36,9 @@ namespace infcl {
 
 constexpr int kWideBM = 64;  // own rows per workgroup
 
-template <int D, bool F16>
+template <int D, bool F16, bool G16>
 __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
+  using GO = GradOut<G16, F16>;  // gradient element type
   constexpr int KS = D / 16;  // 16-wide contraction steps of the full width
   constexpr int KH = KS / 2;  // steps of one wave (half the features)
   constexpr int ROWG = D * 2;
@@ -291,13 +294,13 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
   const bool all_ok = wg0 + kWideBM <= p.own_end;
 #pragma unroll
   for (int o2 = 0; o2 < 2; ++o2) {
-    float* dst = p.dOwn + (wg0 - p.own_off + 32 * o2 + 4 * h) * D + 32 * (wave * FBW) + l32;
+    auto* dst = (typename GO::type*)p.dOwn + (wg0 - p.own_off + 32 * o2 + 4 * h) * D + 32 * (wave * FBW) + l32;
 #pragma unroll
     for (int fbw = 0; fbw < FBW; ++fbw)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int64_t row = wg0 + 32 * o2 + 8 * (r >> 2) + 4 * h + (r & 3);
-        if (all_ok || row < p.own_end) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fbw] = kfin * dacc[o2 * FBW + fbw][r];
+        if (all_ok || row < p.own_end) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fbw] = GO::cvt(kfin * dacc[o2 * FBW + fbw][r]);
       }
   }
 
@@ -341,8 +344,9 @@ __global__ void __launch_bounds__(256, 1) bwd_wide(BwdParams p) {
 // at b = 131072 (192 MiB of swept rows, inside the 256 MiB last-level
 // cache) and 1.5-1.6% faster at b = 163840, 262144 and 1048576, where the
 // tiles come from HBM.
-template <int D, bool F16>
+template <int D, bool F16, bool G16>
 __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
+  using GO = GradOut<G16, F16>;  // gradient element type
   constexpr int KS = D / 16;
   constexpr int KH = KS / 2;
   constexpr int ROWG = D * 2;
@@ -642,13 +646,13 @@ __global__ void __launch_bounds__(256, 1) bwd_wide3(BwdParams p) {
   const bool all_ok = wg0 + kWideBM <= p.own_end;
 #pragma unroll
   for (int o2 = 0; o2 < 2; ++o2) {
-    float* dst = p.dOwn + (wg0 - p.own_off + 32 * o2 + 4 * h) * D + 32 * (wave * FBW) + l32;
+    auto* dst = (typename GO::type*)p.dOwn + (wg0 - p.own_off + 32 * o2 + 4 * h) * D + 32 * (wave * FBW) + l32;
 #pragma unroll
     for (int fbw = 0; fbw < FBW; ++fbw)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int64_t row = wg0 + 32 * o2 + 8 * (r >> 2) + 4 * h + (r & 3);
-        if (all_ok || row < p.own_end) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fbw] = kfin * dacc[o2 * FBW + fbw][r];
+        if (all_ok || row < p.own_end) dst[(8 * (r >> 2) + (r & 3)) * D + 32 * fbw] = GO::cvt(kfin * dacc[o2 * FBW + fbw][r]);
       }
   }
 
@@ -668,22 +672,19 @@ bool bwd_wide_supported(int64_t d, int dtype) { return (dtype == 0 || dtype == 2
 int bwd_wide_workgroups(int64_t nown) { return (int)((nown + kWideBM - 1) / kWideBM); }
 
 int launch_bwd_wide(const BwdParams& p, int nwg, bool f16, hipStream_t stream) {
-  switch (p.d) {
-    case 768:
-      if (f16)
-        hipLaunchKernelGGL((bwd_wide3<768, true>), dim3(nwg), dim3(256), 0, stream, p);
-      else
-        hipLaunchKernelGGL((bwd_wide3<768, false>), dim3(nwg), dim3(256), 0, stream, p);
-      break;
-    case 1024:
-      if (f16)
-        hipLaunchKernelGGL((bwd_wide<1024, true>), dim3(nwg), dim3(256), 0, stream, p);
-      else
-        hipLaunchKernelGGL((bwd_wide<1024, false>), dim3(nwg), dim3(256), 0, stream, p);
-      break;
-    default: return 2;
-  }
-  return hipGetLastError() == hipSuccess ? 0 : 1;
+  auto go = [&](auto f16c, auto g16c) {
+    constexpr bool F = decltype(f16c)::value, G = decltype(g16c)::value;
+    if (p.d == 768)
+      hipLaunchKernelGGL((bwd_wide3<768, F, G>), dim3(nwg), dim3(256), 0, stream, p);
+    else
+      hipLaunchKernelGGL((bwd_wide<1024, F, G>), dim3(nwg), dim3(256), 0, stream, p);
+    return hipGetLastError() == hipSuccess ? 0 : 1;
+  };
+  using T = std::true_type;
+  using N = std::false_type;
+  if (p.d != 768 && p.d != 1024) return 2;
+  if (f16) return p.gdt ? go(T{}, T{}) : go(T{}, N{});
+  return p.gdt ? go(N{}, T{}) : go(N{}, N{});
 }
 
 }  // namespace infcl

@@ -116,9 +116,9 @@ def _fwd(lib, img=A, txt=A, b=64, d=512, dt=0, scale=A, loss=A, loss64=A, lr=A, 
     return lib.infcl_fwd(img, txt, b, d, dt, scale, loss, loss64, lr, lc, aux, ws, wsb, None)
 
 
-def _bwd(lib, img=A, txt=A, b=64, d=512, dt=0, scale=A, lr=A, lc=A, aux=A, dloss=A, di=A, dtx=A, ds=A, ws=A,
+def _bwd(lib, img=A, txt=A, b=64, d=512, dt=0, scale=A, lr=A, lc=A, aux=A, dloss=A, di=A, dtx=A, gdt=1, ds=A, ws=A,
          wsb=1 << 30):
-    return lib.infcl_bwd(img, txt, b, d, dt, scale, lr, lc, aux, dloss, di, dtx, ds, ws, wsb, None)
+    return lib.infcl_bwd(img, txt, b, d, dt, scale, lr, lc, aux, dloss, di, dtx, gdt, ds, ws, wsb, None)
 
 
 @pytest.mark.parametrize("kw,expect", [
@@ -157,6 +157,11 @@ def test_fwd_noalloc_validation(lib, kw, expect):
     (dict(lc=None), infcl.INFCL_ERR_INVALID), (dict(b=-5), infcl.INFCL_ERR_INVALID),
     (dict(d=1536), infcl.INFCL_ERR_UNSUPPORTED), (dict(dt=1, d=768), infcl.INFCL_ERR_UNSUPPORTED),
     (dict(wsb=0), infcl.INFCL_ERR_WORKSPACE),
+    # gradient types: f32, or the inputs' own 16-bit type
+    (dict(gdt=5), infcl.INFCL_ERR_INVALID), (dict(gdt=-1), infcl.INFCL_ERR_INVALID),
+    (dict(gdt=2), infcl.INFCL_ERR_UNSUPPORTED), (dict(dt=2, gdt=0), infcl.INFCL_ERR_UNSUPPORTED),
+    (dict(dt=1, d=256, gdt=0), infcl.INFCL_ERR_UNSUPPORTED), (dict(dt=1, d=256, gdt=2), infcl.INFCL_ERR_UNSUPPORTED),
+    (dict(gdt=0, wsb=0), infcl.INFCL_ERR_WORKSPACE), (dict(dt=2, gdt=2, wsb=0), infcl.INFCL_ERR_WORKSPACE),
 ])
 def test_bwd_validation(lib, kw, expect):
     assert _bwd(lib, **kw) == expect
@@ -173,8 +178,8 @@ def _finish(lib, b=1000, d=512, dt=0, r0=0, bs=1000, nparts=2, cps=A, scale=A, l
     return lib.infcl_fwd_shard_finish(b, d, dt, r0, bs, nparts, cps, scale, lr, lc, aux, lp, ws, wsb, None)
 
 
-def _bwd_shard(lib, b=1000, d=512, dt=0, r0=0, bs=1000, ds=A, di=A, wsb=1 << 30):
-    return lib.infcl_bwd_shard(A, A, b, d, dt, r0, bs, A, A, A, A, None, di, A, ds, A, wsb, None)
+def _bwd_shard(lib, b=1000, d=512, dt=0, r0=0, bs=1000, ds=A, di=A, gdt=1, wsb=1 << 30):
+    return lib.infcl_bwd_shard(A, A, b, d, dt, r0, bs, A, A, A, A, None, di, A, gdt, ds, A, wsb, None)
 
 
 @pytest.mark.parametrize("kw,expect", [

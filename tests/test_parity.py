@@ -177,3 +177,46 @@ def test_widths_between_kernel_widths(d, dtype):
         np.testing.assert_array_equal(gpu[k], padded[k], err_msg=k)
     np.testing.assert_array_equal(gpu["dI"], padded["dI"][:, :d])
     np.testing.assert_array_equal(gpu["dT"], padded["dT"][:, :d])
+
+
+@pytest.mark.parametrize("b,d,dtype", [(777, 512, "bf16"), (700, 768, "bf16"), (600, 1024, "f16"), (513, 384, "f16"),
+                                       (513, 200, "bf16")])
+def test_gradients_in_the_input_type(b, d, dtype):
+    """Gradient type = the inputs' 16-bit type (the 128-row sweep at d = 384
+    and 512, the wide sweeps at 768 and 1024, a zero-padded width at 200): the
+    kernels round the fp32 accumulators once, to nearest even, when storing,
+    so the 16-bit gradients are the fp32 gradients of the same inputs rounded
+    (torch's cast), bit for bit, on the whole batch, on a shard and through
+    the autograd function; dscale does not change."""
+    import torch
+
+    import paper_2410_17243_amd as infcl
+    from gpu_util import device_inputs
+
+    img, txt = synth.clip_pairs(b, d, 1.0, seed=b + d, dtype=dtype)
+    I, T = device_inputs(img, txt, dtype)
+    sc = torch.tensor([f32_scale(14.29)], dtype=torch.float32, device=I.device)
+    f = infcl.clip_loss_fwd(I, T, sc)
+    dl = torch.tensor([0.7], dtype=torch.float32, device=I.device)
+    g32 = infcl.clip_loss_bwd(I, T, sc, f, dloss=dl)
+    g16 = infcl.clip_loss_bwd(I, T, sc, f, dloss=dl, grad_dtype=I.dtype)
+    assert g16[0].dtype == g16[1].dtype == I.dtype
+    assert torch.equal(g16[0], g32[0].to(I.dtype)) and torch.equal(g16[1], g32[1].to(I.dtype))
+    assert torch.equal(g16[2], g32[2])
+    # a shard of own rows [64, 64 + 300)
+    r0, bs = 64, 300
+    ds = torch.empty((), dtype=torch.float64, device=I.device)
+    s32 = [torch.empty((bs, d), dtype=torch.float32, device=I.device) for _ in range(2)]
+    s16 = [torch.empty((bs, d), dtype=I.dtype, device=I.device) for _ in range(2)]
+    for out in (s32, s16):
+        infcl.infcl_bwd_shard(I, T, sc.reshape(()), r0, bs, f["lse_r"], f["lse_c"], f["aux"], None, out[0], out[1], ds,
+                              f["workspace"])
+    assert torch.equal(s16[0], s32[0].to(I.dtype)) and torch.equal(s16[1], s32[1].to(I.dtype))
+    # the autograd function returns gradients in the inputs' dtype
+    Ia, Ta = I.clone().requires_grad_(), T.clone().requires_grad_()
+    sa = sc.reshape(()).clone().requires_grad_()
+    infcl.clip_loss(Ia, Ta, sa).backward()
+    ref = infcl.clip_loss_bwd(I, T, sc, f)
+    assert Ia.grad.dtype == I.dtype
+    assert torch.equal(Ia.grad, ref[0].to(I.dtype)) and torch.equal(Ta.grad, ref[1].to(I.dtype))
+    torch.cuda.synchronize()
