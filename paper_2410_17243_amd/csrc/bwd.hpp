@@ -27,8 +27,11 @@ struct BwdParams {
 constexpr int kBwdBN = kSweepBN;  // swept rows per tile
 
 // Gradient element type of a sweep: fp32, or with G16 the 16-bit input type
-// (fp16 with F16, else bf16), rounded to nearest even from the fp32
-// accumulator once, when stored.
+// (fp16 with F16, else bf16), rounded to nearest even from the fp32 gradient
+// when stored.  The fp32 value is materialised first: the compiler would
+// otherwise fuse the final scaling into an fp16 conversion (a mixed-precision
+// multiply that rounds the exact product once), whose result differs from a
+// cast of the fp32 gradient by one unit where that lands on a tie.
 template <bool G16, bool F16>
 struct GradOut {
   using type = float;
@@ -37,7 +40,10 @@ struct GradOut {
 template <bool F16>
 struct GradOut<true, F16> {
   using type = __bf16;
-  static __device__ __forceinline__ __bf16 cvt(float v) { return to16<F16>(v); }
+  static __device__ __forceinline__ __bf16 cvt(float v) {
+    asm volatile("" : "+v"(v));
+    return to16<F16>(v);
+  }
 };
 
 }  // namespace infcl
