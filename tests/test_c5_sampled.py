@@ -1,7 +1,7 @@
 """Parity at b = 4194304 (d = 768, s = 14.29: one GPU's full CLIP-ViT-L/14-shaped
 batch) on the generator's inputs, against the exact sampled oracle.
 
-About 100 s on the GPU machine, most of it drawing the 6.4 billion input values
+About 100 s on an MI355X host, most of it drawing the 6.4 billion input values
 and their fp64 copies (about 70 GB of host memory).  What it checks:
   * the whole forward: r_i, r_i - x_ii for 96 seeded rows and c_j, c_j - x_jj
     for 96 seeded columns against the sampled oracle (independent of the GPU),
