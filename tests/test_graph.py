@@ -11,8 +11,10 @@ from gpu_util import device_inputs, synth
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("b,d,dtype", [(1000, 512, "bf16"), (777, 768, "bf16"), (600, 256, "f16")])
-def test_captured_step_replays_bitwise(b, d, dtype):
+@pytest.mark.parametrize("b,d,dtype,grad16", [(1000, 512, "bf16", False), (777, 768, "bf16", False),
+                                              (600, 256, "f16", False),
+                                              (513, 200, "bf16", True)])  # padded width, bf16 gradients
+def test_captured_step_replays_bitwise(b, d, dtype, grad16):
     img, txt = synth.clip_pairs(b, d, 1.0, seed=31, dtype=dtype)
     I, T = device_inputs(img, txt, dtype)
     dev = I.device
@@ -25,8 +27,8 @@ def test_captured_step_replays_bitwise(b, d, dtype):
         "lse_r": torch.empty(b, dtype=torch.float32, device=dev),
         "lse_c": torch.empty(b, dtype=torch.float32, device=dev),
         "aux": torch.empty(3 * b, dtype=torch.float32, device=dev),
-        "dimg": torch.empty((b, d), dtype=torch.float32, device=dev),
-        "dtxt": torch.empty((b, d), dtype=torch.float32, device=dev),
+        "dimg": torch.empty((b, d), dtype=I.dtype if grad16 else torch.float32, device=dev),
+        "dtxt": torch.empty((b, d), dtype=I.dtype if grad16 else torch.float32, device=dev),
         "dscale": torch.empty((), dtype=torch.float32, device=dev),
     }
 
